@@ -1,0 +1,180 @@
+"""Benchmark of the batched candidate-scoring path on one MI355X.
+
+Workload: the dataset-scale configuration -- 600 GEMM problems x 8,192
+candidate configurations = 4,915,200 rows, 128 features, a random GBDT of
+2,000 depth-10 trees and a random MLP 128->512->512->256->1 -- all synthetic
+and seeded (see synth/).  One step is one pass of the whole path over that
+batch, inputs already resident in HBM:
+
+    features -> forest score -> top-10 per problem -> regret
+             -> MLP score    -> top-10 per problem -> regret
+
+Prints ONE JSON line (rank 0).  `value` = rows per second through the whole
+step.  Per-stage times come from HIP events recorded on the launch stream
+inside the timed region.  `roofline` is for the dominant kernel (forest
+scoring); `cpu_baseline` times the CPU oracle on a bounded sample of the same
+workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "candidate rows scored/sec (features+forest+top-k) at 4.9M rows; % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+# VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+LANE_OPS_PER_S = 256 * 64 * 2.4e9
+# an exact traversal step issues at least 4 VALU lane-ops per node visit
+# (child index, node address, feature address, compare)
+MIN_OPS_PER_VISIT = 4
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, n_problems: int) -> dict:
+    import oracle
+    cfg = w.cfg
+    seg = w.seg[: n_problems + 1]
+    R = int(seg[-1])
+    probs = w.problems[:n_problems]
+    cands = {k: v[:R] for k, v in w.cands.items()}
+    import synth
+    m = synth.mlp(synth.CONFIGS["mlp"])
+    t0 = time.perf_counter()
+    X = oracle.features(w.hw, probs, seg, cands, cfg.n_features)
+    s = oracle.forest(w.forest, X)
+    idx, _ = oracle.topk(s, seg, cfg.k)
+    oracle.regret(w.runtimes[:R], seg, idx)
+    sm = oracle.mlp(m, X)
+    idx2, _ = oracle.topk(sm, seg, cfg.k)
+    oracle.regret(w.runtimes[:R], seg, idx2)
+    dt = time.perf_counter() - t0
+    return {"value": R / dt, "unit": "rows/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"first {n_problems} of {cfg.n_problems} problems ({R} rows), whole path "
+                      f"(features, forest, MLP, top-{cfg.k}, regret), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--cpu-problems", type=int, default=64,
+                    help="problems in the oracle's timed sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {a.gpus}); "
+              "the path shards by problem segment across GPUs, which is not built here.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2609_35587_amd import hwsel
+
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    log("generate workload")
+    w = synth.workload("dataset")
+    mw = synth.mlp(synth.CONFIGS["mlp"])
+    cfg = w.cfg
+    R, P, F, k = cfg.rows, cfg.n_problems, cfg.n_features, cfg.k
+    probs = hwsel.to_device(w.problems, dev)
+    seg = hwsel.to_device(w.seg, dev)
+    cands = {n: hwsel.to_device(v, dev) for n, v in w.cands.items()}
+    rt = hwsel.to_device(w.runtimes, dev)
+    forest = dict(w.forest)
+    for n in ("node_feature", "node_threshold", "leaf_value"):
+        forest[n] = hwsel.to_device(w.forest[n], dev)
+    mlp = {n: hwsel.to_device(v, dev) for n, v in mw.items()}
+    X = torch.empty((R, F), dtype=torch.float32, device=dev)
+    s_f = torch.empty(R, dtype=torch.float32, device=dev)
+    s_m = torch.empty(R, dtype=torch.float32, device=dev)
+    outs = [(torch.empty((P, k), dtype=torch.int32, device=dev), torch.empty((P, k), dtype=torch.float32, device=dev))
+            for _ in range(2)]
+    regs = [tuple(torch.empty(P, dtype=dt, device=dev) for dt in (torch.float32, torch.float32, torch.int32))
+            for _ in range(2)]
+    stream = torch.cuda.current_stream()
+    stages = ["features", "forest", "topk_forest", "regret_forest", "mlp", "topk_mlp", "regret_mlp"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        hwsel.hwsel_features(w.hw, probs, seg, cands, F, X=X)
+        mark(1)
+        hwsel.hwsel_forest_score(forest, X, scores=s_f)
+        mark(2)
+        hwsel.hwsel_topk_per_problem(s_f, seg, k, idx=outs[0][0], vals=outs[0][1])
+        mark(3)
+        hwsel.hwsel_regret(rt, seg, outs[0][0], *regs[0])
+        mark(4)
+        hwsel.hwsel_mlp_score(mlp, X, scores=s_m)
+        mark(5)
+        hwsel.hwsel_topk_per_problem(s_m, seg, k, idx=outs[1][0], vals=outs[1][1])
+        mark(6)
+        hwsel.hwsel_regret(rt, seg, outs[1][0], *regs[1])
+        mark(7)
+
+    log(f"warmup {a.warmup}")
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"timed {a.steps}")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step(evs[i])
+        log(f"  step {i + 1} enqueued")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_stage = {name: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, name in enumerate(stages)}
+    ms_step = float(np.mean([e[0].elapsed_time(e[7]) for e in evs]))
+    log(f"stages ms {per_stage}  step {ms_step:.3f} ms  wall/step {1e3 * wall / a.steps:.3f} ms")
+
+    # roofline of the dominant kernel (forest scoring): node visits per launch
+    visits = R * cfg.trees * cfg.depth
+    t_forest = per_stage["forest"] / 1e3
+    visit_rate = visits / t_forest
+    peak_visits = LANE_OPS_PER_S / MIN_OPS_PER_VISIT
+    # algorithmic HBM bytes of the whole step: candidate records (17 B) + X write
+    # (4F) + X read by forest and MLP (2 x 4F) + two score vectors written and
+    # read (4 x 4 B) + runtimes read twice (2 x 4 B)
+    step_bytes = R * (17 + 3 * 4 * F + 16 + 8)
+    hbm_gbs = step_bytes / (ms_step / 1e3) / 1e9
+    forest_bytes = R * (4 * F + 4)
+    line = {
+        "metric": METRIC, "value": R / (ms_step / 1e3), "unit": "rows/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "dataset-scale: 600 problems x 8192 candidates = 4915200 rows, 128 features, "
+                               "GBDT 2000 trees depth 10 + MLP 128-512-512-256-1 (bf16), top-10 + regret",
+                   "rows": R, "problems": P, "features": F, "trees": cfg.trees, "depth": cfg.depth, "k": k},
+        "stages_ms": per_stage,
+        "hbm_roofline_step": {"achieved": hbm_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": hbm_gbs / HBM_PEAK_GBS, "bytes_per_row": step_bytes / R},
+        "roofline": {"kernel": "forest_score", "bound": "alu", "achieved": visit_rate / 1e9,
+                     "peak": peak_visits / 1e9, "unit": "Gvisits/s", "frac": visit_rate / peak_visits,
+                     "traffic": None, "visits_per_launch": visits,
+                     "hbm_frac": forest_bytes / t_forest / 1e9 / HBM_PEAK_GBS},
+    }
+    if not a.no_cpu_baseline:
+        log(f"cpu baseline: oracle on {a.cpu_problems} problems")
+        line["cpu_baseline"] = cpu_baseline(w, a.cpu_problems)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

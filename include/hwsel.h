@@ -1,0 +1,226 @@
+/*
+ * hwsel.h -- C ABI of the batched candidate-scoring library for MI355X (gfx950).
+ *
+ * The library ranks GEMM kernel configurations without running them, as in
+ * "Hardware-Aware Features for CUTLASS Kernel Selection": every
+ * (problem p, candidate c) row gets a statically computed feature vector
+ * x = phi(p, c, h) for a target hardware description h; a learned scorer
+ * f maps rows to scores; the deployed choice per problem is the
+ * highest-scoring candidate; the choice is judged by its selection regret.
+ *
+ * Conventions for every entry point
+ *   - Array arguments are DEVICE pointers (memory of the current HIP device)
+ *     unless the comment says "host".  The caller owns every buffer; the
+ *     library allocates nothing, frees nothing and keeps no device state.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *     Calls only enqueue work on it: they return before the work finishes and
+ *     never synchronise.
+ *   - Arguments are checked on the host before anything is enqueued.  A
+ *     rejected call returns a non-zero status, enqueues nothing and records a
+ *     message readable with hwsel_last_error() (per thread).  Device-resident
+ *     contents (offsets, indices, knob values) cannot be checked without a
+ *     synchronisation; each call states what it assumes of them and what the
+ *     kernels do when the assumption is broken (they never read or write out
+ *     of the stated bounds).
+ *   - All entry points are thread-safe.
+ */
+#ifndef HWSEL_H
+#define HWSEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HWSEL_OK = 0,
+    HWSEL_EINVAL = 1,       /* a null pointer, a size out of range, misalignment */
+    HWSEL_EUNSUPPORTED = 2, /* a valid request this build does not implement */
+    HWSEL_EHIP = 3          /* the HIP runtime reported an error at launch */
+} hwsel_status;
+
+/* Integer codes used in problem and candidate records. */
+enum { HWSEL_LAYOUT_TN = 0, HWSEL_LAYOUT_TT = 1, HWSEL_LAYOUT_NN = 2, HWSEL_LAYOUT_NT = 3 };
+enum { HWSEL_DTYPE_BF16 = 0, HWSEL_DTYPE_FP16 = 1, HWSEL_DTYPE_FP8 = 2, HWSEL_DTYPE_FP32 = 3 };
+enum { HWSEL_KS_WS = 0, HWSEL_KS_PINGPONG = 1, HWSEL_KS_COOPERATIVE = 2 };
+enum { HWSEL_ES_NOSMEM = 0, HWSEL_ES_TMA = 1, HWSEL_ES_TMA_COOPERATIVE = 2 };
+enum { HWSEL_TS_PERSISTENT = 0, HWSEL_TS_STREAMK = 1 };
+
+/*
+ * Hardware descriptor h of the TARGET the ranked kernels would run on
+ * (section "Structural Core": SM count, shared-memory and register-file
+ * capacity per SM, LLC capacity, HBM bandwidth, peak throughput of the
+ * compute engine).  Exact integers in fixed units: bytes, GB/s (= bytes per
+ * ns), GFLOP/s (= flop per ns).  peak_gflops is indexed by the input dtype
+ * code (bf16, fp16, fp8).  Passed by value.  Every field must be >= 1 except
+ * smem_reserved (>= 0); hwsel_features rejects other values.
+ */
+typedef struct hwsel_hw {
+    int64_t n_sm, smem_per_sm, smem_per_block_max, smem_reserved;
+    int64_t regs_per_sm, max_regs_per_thread, max_blocks_per_sm, max_threads_per_sm;
+    int64_t arch_id, llc_bytes, hbm_bw_gbps;
+    int64_t peak_gflops[3];
+} hwsel_hw_t;
+
+/*
+ * GEMM problem p = (M, N, K, layout) with its input dtype (section "Problem
+ * and Candidate Sets").  The layout tag names the storage of A, then of B,
+ * as in the printed kernel's TN = A row-major, B column-major: NN and NT
+ * have A column-major; TT and NT have B row-major.  16 bytes per record,
+ * array-of-structs on the device.
+ */
+typedef struct hwsel_problem {
+    int32_t M, N, K;
+    uint8_t layout, dtype, pad[2];
+} hwsel_problem_t;
+
+/*
+ * Candidate configurations c, one row each, as a struct of DEVICE arrays of
+ * length R (section "Configuration Space", Table "Configuration knobs"):
+ * tile shape (T_M, T_N, T_K), instruction tile (16*inst_m_div16, inst_n,
+ * inst_k), pipeline stages, cluster (C_M, C_N), swizzle, mainloop schedule,
+ * epilogue schedule and tile scheduler codes.  The struct itself is read on
+ * the host.  Knob values of 0 are read as 1; schedule codes beyond the last
+ * one are read as the last one.
+ */
+typedef struct hwsel_cands {
+    const uint16_t *tile_m, *tile_n, *tile_k, *inst_n;
+    const uint8_t *stages, *cluster_m, *cluster_n, *swizzle, *inst_m_div16, *inst_k;
+    const uint8_t *kernel_sched, *epi_sched, *tile_sched;
+} hwsel_cands_t;
+
+/*
+ * Features.  X[r][0..n_features) = phi(p(r), c_r, h) for every row r < R,
+ * where p(r) is the problem whose segment [seg_offsets[p], seg_offsets[p+1])
+ * holds r (section "Feature Map", Table "Feature groups", and the formulas of
+ * "Work Decomposition and Wave Quantization", "Memory Behavior", "Resource
+ * Pressure and Occupancy", "Pipeline Balance").  n_features is 64, 96 or 128;
+ * the 96- and 128-column schemas extend the 64-column one.
+ *
+ *   problems     [P] records; M, N, K below 1 are read as 1.
+ *   seg_offsets  [P+1] int64, non-decreasing, seg_offsets[0] = 0,
+ *                seg_offsets[P] = R (assumed; a row outside every segment is
+ *                assigned to the nearest one, never read out of bounds).
+ *   X            fp32, row-major, leading dimension ld >= n_features,
+ *                ld % 4 == 0, 16-byte aligned.
+ * Integer-valued columns are exact integers rounded once to fp32; ratio
+ * columns are one binary64 division of exact integers rounded to fp32; the
+ * log2 columns are binary64 log2 rounded to fp32.
+ * Returns HWSEL_EINVAL for null pointers, P < 1, R < 1, a bad ld or alignment
+ * or hardware field; HWSEL_EUNSUPPORTED for another n_features.
+ */
+int hwsel_features(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P,
+                   const int64_t *seg_offsets, const hwsel_cands_t *cands, int64_t R,
+                   int32_t n_features, float *X, int64_t ld, void *stream);
+
+/*
+ * Additive tree ensemble f(x) = base_score + sum_t leaf_t(x) (section
+ * "Model A (gradient-boosted ranker)").  n_trees perfect binary trees of the
+ * same depth, stored breadth-first per tree: internal node i (0-based) has
+ * children 2i+1 (left) and 2i+2 (right); a row goes left iff
+ * x[node_feature] < node_threshold, or x is NaN and flags bit 0 is set.
+ * Device arrays: node_feature uint8 [n_trees][2^depth - 1] (values must be
+ * < n_features; larger ones are read as n_features - 1), node_threshold fp32
+ * [n_trees][2^depth - 1], leaf_value fp32 [n_trees][2^depth].
+ * The struct itself is read on the host.
+ */
+typedef struct hwsel_forest {
+    int32_t n_trees, depth, n_features;
+    uint32_t flags;                /* bit 0: NaN goes left */
+    float base_score;
+    const uint8_t *node_feature;
+    const float *node_threshold;
+    const float *leaf_value;
+} hwsel_forest_t;
+
+/*
+ * scores[r] = f(X[r]) for r < R, accumulated in fp32 in a fixed order (the
+ * same inputs give bit-identical scores from run to run).
+ *   X: fp32 [R][ld], ld >= n_features, as written by hwsel_features.
+ * Returns HWSEL_EINVAL for null pointers, R < 1, n_trees < 1, ld <
+ * n_features; HWSEL_EUNSUPPORTED for depth outside [1, 12] or n_features
+ * outside [1, 256].
+ */
+int hwsel_forest_score(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld,
+                       float *scores, void *stream);
+
+/*
+ * Leaf index of every tree for selected rows: leaf_idx[i][t] = index in
+ * [0, 2^depth) of the leaf that row rows[i] reaches in tree t.  A check
+ * hook for the traversal (same decision rule as hwsel_forest_score).
+ *   rows: int64 [n_rows] (values must lie in [0, R); others are clamped).
+ * Same status codes as hwsel_forest_score.
+ */
+int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld,
+                        const int64_t *rows, int64_t n_rows, uint16_t *leaf_idx, void *stream);
+
+/*
+ * Feed-forward ranker (section "Model B (feed-forward ranker)") with widths
+ * 128 -> 512 -> 512 -> 256 -> 1 and GELU hidden activations:
+ *   h0 = bf16((clean(x) - mean) * inv_std)   (fp32, two operations; clean maps
+ *                                            NaN and +-inf to 0)
+ *   h_l = bf16(GELU(W_l h_{l-1} + b_l)), l = 1..3, fp32 accumulation
+ *   score = W4 h3 + b4 in fp32.
+ * Device arrays: mean, inv_std fp32 [128]; W1 [512][128], W2 [512][512],
+ * W3 [256][512], W4 [1][256] as bf16 bit patterns (uint16), row-major
+ * [out][in]; b1..b4 fp32.  The struct itself is read on the host.
+ */
+typedef struct hwsel_mlp {
+    int32_t n_in, h1, h2, h3;
+    const float *mean, *inv_std;
+    const uint16_t *W1, *W2, *W3, *W4;
+    const float *b1, *b2, *b3, *b4;
+} hwsel_mlp_t;
+
+/*
+ * scores[r] = MLP(X[r][0..128)) for r < R.  X: fp32 [R][ld], ld >= 128,
+ * ld % 4 == 0, 16-byte aligned.  Returns HWSEL_EINVAL for null pointers,
+ * R < 1, bad ld/alignment; HWSEL_EUNSUPPORTED for other widths.
+ */
+int hwsel_mlp_score(const hwsel_mlp_t *m, const float *X, int64_t R, int64_t ld, float *scores,
+                    void *stream);
+
+/*
+ * Per-problem selection, eq. (selection) generalised to the k best:
+ * idx[p][j] = local index (0-based within segment p) of the candidate ranked
+ * j-th by score descending, ties broken by the lower index; -0 equals +0;
+ * NaN ranks below -inf.  Segments with fewer than k rows are padded with
+ * index -1 and value -inf.  vals (nullable) receives the scores.
+ *   scores [R] fp32 with R = seg_offsets[P]; idx int32 [P][k]; vals fp32 [P][k].
+ *   seg_offsets as for hwsel_features (segments longer than 2^31 - 1 rows are
+ *   not supported).
+ * Returns HWSEL_EINVAL for null pointers, P < 1, k outside [1, 64].
+ */
+int hwsel_topk_per_problem(const float *scores, const int64_t *seg_offsets, int32_t P, int32_t k,
+                           int32_t *idx, float *vals, void *stream);
+
+/*
+ * Selection regret, eq. (regret): within a problem the flop count is fixed,
+ * so T(c) / T_best = t_best / t(c) for runtimes t.  For each problem p:
+ *   t_best          = min runtime of the segment,
+ *   regret_top1[p]  = 1 - t_best / t(idx[p][0])          (binary64, then fp32),
+ *   regret_bestk[p] = 1 - t_best / min_j t(idx[p][j])    (nullable),
+ *   best_idx[p]     = local index of t_best, lowest on ties (nullable).
+ * Equal runtimes (inf included) give exactly 0; NaN runtimes rank above +inf;
+ * an empty segment or a -1 pick gives NaN and best_idx -1.
+ *   runtimes [R] fp32 (seconds), idx int32 [P][k] as from
+ *   hwsel_topk_per_problem (entries outside [-1, segment length) are read as
+ *   -1).
+ * Returns HWSEL_EINVAL for null pointers, P < 1, k outside [1, 64].
+ */
+int hwsel_regret(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx,
+                 int32_t k, float *regret_top1, float *regret_bestk, int32_t *best_idx,
+                 void *stream);
+
+/* Static text for a status code. */
+const char *hwsel_status_string(int status);
+/* Detail of the last failed call on this thread ("" if none). */
+const char *hwsel_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HWSEL_H */

@@ -1,0 +1,152 @@
+// C-ABI entry points: host-side argument checks, then one launch each.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "internal.hpp"
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int status, const char *fn, const char *fmt, ...) __attribute__((format(printf, 3, 4)));
+
+int fail(int status, const char *fn, const char *fmt, ...)
+{
+    int n = snprintf(g_err, sizeof g_err, "%s: ", fn);
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err + n, sizeof g_err - (size_t)n, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int launched(hipError_t e, const char *fn)
+{
+    if (e != hipSuccess) return fail(HWSEL_EHIP, fn, "launch failed: %s", hipGetErrorString(e));
+    g_err[0] = 0;
+    return HWSEL_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char *hwsel_status_string(int status)
+{
+    switch (status) {
+    case HWSEL_OK: return "ok";
+    case HWSEL_EINVAL: return "invalid argument";
+    case HWSEL_EUNSUPPORTED: return "unsupported";
+    case HWSEL_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+const char *hwsel_last_error(void) { return g_err; }
+
+int hwsel_features(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                   const hwsel_cands_t *cands, int64_t R, int32_t n_features, float *X, int64_t ld,
+                   void *stream)
+{
+    static const char *fn = "hwsel_features";
+    if (!problems || !seg_offsets || !cands || !X) return fail(HWSEL_EINVAL, fn, "null pointer");
+    const void *fields[] = {cands->tile_m, cands->tile_n, cands->tile_k, cands->inst_n, cands->stages,
+                            cands->cluster_m, cands->cluster_n, cands->swizzle, cands->inst_m_div16,
+                            cands->inst_k, cands->kernel_sched, cands->epi_sched, cands->tile_sched};
+    for (const void *f : fields)
+        if (!f) return fail(HWSEL_EINVAL, fn, "null candidate field");
+    if (P < 1 || R < 1) return fail(HWSEL_EINVAL, fn, "P=%d R=%lld must be >= 1", P, (long long)R);
+    if (n_features != 64 && n_features != 96 && n_features != 128)
+        return fail(HWSEL_EUNSUPPORTED, fn, "n_features=%d (supported: 64, 96, 128)", n_features);
+    if (ld < n_features || ld % 4 != 0) return fail(HWSEL_EINVAL, fn, "ld=%lld", (long long)ld);
+    if (!aligned16(X)) return fail(HWSEL_EINVAL, fn, "X not 16-byte aligned");
+    const int64_t positive[] = {hw.n_sm, hw.smem_per_sm, hw.smem_per_block_max, hw.regs_per_sm,
+                                hw.max_regs_per_thread, hw.max_blocks_per_sm, hw.max_threads_per_sm,
+                                hw.arch_id, hw.llc_bytes, hw.hbm_bw_gbps, hw.peak_gflops[0],
+                                hw.peak_gflops[1], hw.peak_gflops[2]};
+    for (int64_t v : positive)
+        if (v < 1) return fail(HWSEL_EINVAL, fn, "hardware field %lld < 1", (long long)v);
+    if (hw.smem_reserved < 0) return fail(HWSEL_EINVAL, fn, "smem_reserved < 0");
+    const hwsel::HwDev h{hw.n_sm, hw.smem_per_sm, hw.smem_per_block_max, hw.smem_reserved, hw.regs_per_sm,
+                         hw.max_regs_per_thread, hw.max_blocks_per_sm, hw.max_threads_per_sm, hw.arch_id,
+                         hw.llc_bytes, hw.hbm_bw_gbps, {hw.peak_gflops[0], hw.peak_gflops[1], hw.peak_gflops[2]}};
+    const hwsel::CandsDev c{cands->tile_m, cands->tile_n, cands->tile_k, cands->inst_n, cands->stages,
+                            cands->cluster_m, cands->cluster_n, cands->swizzle, cands->inst_m_div16,
+                            cands->inst_k, cands->kernel_sched, cands->epi_sched, cands->tile_sched};
+    return launched(hwsel::launch_features(h, problems, P, seg_offsets, c, R, n_features, X, ld,
+                                           (hipStream_t)stream),
+                    fn);
+}
+
+static int check_forest(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld, const char *fn)
+{
+    if (!f || !X || !f->node_feature || !f->node_threshold || !f->leaf_value)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (R < 1 || f->n_trees < 1) return fail(HWSEL_EINVAL, fn, "R=%lld n_trees=%d", (long long)R, f->n_trees);
+    if (f->depth < 1 || f->depth > 12) return fail(HWSEL_EUNSUPPORTED, fn, "depth=%d (1..12)", f->depth);
+    if (f->n_features < 1 || f->n_features > 256)
+        return fail(HWSEL_EUNSUPPORTED, fn, "n_features=%d (1..256)", f->n_features);
+    if (ld < f->n_features) return fail(HWSEL_EINVAL, fn, "ld=%lld < n_features", (long long)ld);
+    return HWSEL_OK;
+}
+
+int hwsel_forest_score(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld, float *scores,
+                       void *stream)
+{
+    static const char *fn = "hwsel_forest_score";
+    if (int s = check_forest(f, X, R, ld, fn)) return s;
+    if (!scores) return fail(HWSEL_EINVAL, fn, "null scores");
+    return launched(hwsel::launch_forest_score(*f, X, R, ld, scores, (hipStream_t)stream), fn);
+}
+
+int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld, const int64_t *rows,
+                        int64_t n_rows, uint16_t *leaf_idx, void *stream)
+{
+    static const char *fn = "hwsel_forest_leaves";
+    if (int s = check_forest(f, X, R, ld, fn)) return s;
+    if (!rows || !leaf_idx) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (n_rows < 1) return fail(HWSEL_EINVAL, fn, "n_rows=%lld", (long long)n_rows);
+    return launched(hwsel::launch_forest_leaves(*f, X, R, ld, rows, n_rows, leaf_idx, (hipStream_t)stream), fn);
+}
+
+int hwsel_mlp_score(const hwsel_mlp_t *m, const float *X, int64_t R, int64_t ld, float *scores, void *stream)
+{
+    static const char *fn = "hwsel_mlp_score";
+    if (!m || !X || !scores || !m->mean || !m->inv_std || !m->W1 || !m->W2 || !m->W3 || !m->W4 || !m->b1 ||
+        !m->b2 || !m->b3 || !m->b4)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (m->n_in != 128 || m->h1 != 512 || m->h2 != 512 || m->h3 != 256)
+        return fail(HWSEL_EUNSUPPORTED, fn, "widths %d-%d-%d-%d (supported: 128-512-512-256)", m->n_in, m->h1,
+                    m->h2, m->h3);
+    if (R < 1) return fail(HWSEL_EINVAL, fn, "R=%lld", (long long)R);
+    if (ld < 128 || ld % 4 != 0) return fail(HWSEL_EINVAL, fn, "ld=%lld", (long long)ld);
+    if (!aligned16(X)) return fail(HWSEL_EINVAL, fn, "X not 16-byte aligned");
+    return launched(hwsel::launch_mlp(*m, X, R, ld, scores, (hipStream_t)stream), fn);
+}
+
+int hwsel_topk_per_problem(const float *scores, const int64_t *seg_offsets, int32_t P, int32_t k, int32_t *idx,
+                           float *vals, void *stream)
+{
+    static const char *fn = "hwsel_topk_per_problem";
+    if (!scores || !seg_offsets || !idx) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1) return fail(HWSEL_EINVAL, fn, "P=%d", P);
+    if (k < 1 || k > 64) return fail(HWSEL_EINVAL, fn, "k=%d (1..64)", k);
+    return launched(hwsel::launch_topk(scores, seg_offsets, P, k, idx, vals, (hipStream_t)stream), fn);
+}
+
+int hwsel_regret(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx, int32_t k,
+                 float *regret_top1, float *regret_bestk, int32_t *best_idx, void *stream)
+{
+    static const char *fn = "hwsel_regret";
+    if (!runtimes || !seg_offsets || !idx || !regret_top1) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1) return fail(HWSEL_EINVAL, fn, "P=%d", P);
+    if (k < 1 || k > 64) return fail(HWSEL_EINVAL, fn, "k=%d (1..64)", k);
+    return launched(hwsel::launch_regret(runtimes, seg_offsets, P, idx, k, regret_top1, regret_bestk, best_idx,
+                                         (hipStream_t)stream),
+                    fn);
+}
+
+}  // extern "C"

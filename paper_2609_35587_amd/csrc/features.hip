@@ -1,0 +1,281 @@
+// Feature kernel: x = phi(p, c, h) for every (problem, candidate) row.
+//
+// One thread per row; a wave owns 64 consecutive rows.  The candidate record
+// is read as coalesced struct-of-arrays streams (17 B/row), the problem record
+// once per row from a tiny L2-resident table.  The feature row is built in
+// registers, then staged through LDS 32 columns at a time so that every
+// global store is a 16-byte vector store into a contiguous 128-byte row
+// segment (8 rows per wave instruction).  The kernel is bound by the X write
+// stream (4F bytes per row).
+//
+// Numeric contract (same as the definition the oracle follows):
+//   integer columns  - exact int64 values, one conversion to fp32 (RNE);
+//   ratio columns    - one binary64 division of two exact int64 values, then
+//                      fp32 (the division is correctly rounded on gfx950);
+//   composite columns- a fixed short sequence of binary64 operations;
+//   log2 columns     - binary64 log2, then fp32.
+// This translation unit is compiled with -ffp-contract=off so no multiply-add
+// is fused behind the sequence's back.
+#include "internal.hpp"
+
+#include <math.h>
+
+namespace hwsel {
+namespace {
+
+__device__ __forceinline__ int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+__device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ float exact(int64_t v) { return (float)v; }
+__device__ __forceinline__ float quot(int64_t n, int64_t d) { return (float)((double)n / (double)d); }
+__device__ __forceinline__ float lg(int64_t v) { return (float)log2((double)v); }
+
+// Knob codes.
+constexpr int kWS = 0, kCoop = 2;
+constexpr int eNone = 0, eTma = 1;
+constexpr int tStreamK = 1;
+constexpr int dFp16 = 1, dFp8 = 2, dFp32 = 3;
+constexpr int lNN = 2, lNT = 3, lTT = 1;
+
+template <int F>
+__device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, const CandsDev &c,
+                                    int64_t r, float (&x)[F])
+{
+    // ---- problem ----
+    const int64_t M = max64(pb.M, 1), N = max64(pb.N, 1), K = max64(pb.K, 1);
+    const int layout = pb.layout < 3 ? pb.layout : 3;
+    const int dtype = pb.dtype < 2 ? pb.dtype : 2;
+    const int64_t eb = dtype == dFp8 ? 1 : 2;          // input element bytes (A and B)
+    const int64_t ob = 2;                              // output / C element bytes
+    const int out_dtype = dtype == dFp16 ? dFp16 : 0;
+    const int64_t pk = h.peak[dtype];
+
+    // ---- candidate ----
+    const int64_t tm = max64(c.tile_m[r], 1), tn = max64(c.tile_n[r], 1), tk = max64(c.tile_k[r], 1);
+    const int64_t in_ = max64(c.inst_n[r], 1);
+    const int64_t st = max64(c.stages[r], 1);
+    const int64_t cm = max64(c.cluster_m[r], 1), cn = max64(c.cluster_n[r], 1);
+    const int64_t swz = c.swizzle[r];
+    const int64_t im = 16 * max64(c.inst_m_div16[r], 1), ik = max64(c.inst_k[r], 1);
+    const int ks = c.kernel_sched[r] < 2 ? c.kernel_sched[r] : 2;
+    const int es = c.epi_sched[r] < 2 ? c.epi_sched[r] : 2;
+    const int ts = c.tile_sched[r] < 1 ? c.tile_sched[r] : 1;
+
+    // ---- schedule: warpgroups ----
+    const int64_t threads = ks == kWS ? 256 : 384;     // producer + 1 or 2 consumer warpgroups
+    const int64_t consumers = ks == kCoop ? 2 : 1;     // consumer warpgroups on one tile
+
+    // ---- work decomposition ----
+    const int64_t gm = cdiv64(M, tm), gn = cdiv64(N, tn), gk = cdiv64(K, tk);
+    const int64_t ntile = gm * gn;
+
+    // ---- shared memory, registers, residency ----
+    const int64_t stage_bytes = (tm + tn) * tk * eb;
+    const int64_t main_bytes = st * stage_bytes;
+    const int64_t frag = min64(tm, 64) * min64(tn, 32) * ob;
+    const int64_t epi_bytes = es == eNone ? 0 : (es == eTma ? 2 * frag : 4 * frag);
+    const int64_t smem = (ks == kWS ? max64(main_bytes, epi_bytes) : main_bytes + epi_bytes) + h.smem_rsv;
+    const int64_t by_smem = h.smem_sm / smem;
+    const int64_t regs = min64(h.regs_thread_max, cdiv64(tm * tn, threads) + 32);
+    const int64_t by_regs = h.regs_sm / (regs * threads);
+    const int64_t by_arch = min64(h.blocks_sm_max, h.threads_sm_max / threads);
+    const int64_t resident = min64(min64(by_smem, by_regs), by_arch);
+    const bool fits = main_bytes + epi_bytes + h.smem_rsv <= h.smem_block;
+
+    // ---- waves over resident slots ----
+    const int64_t slot_count = h.n_sm * (resident > 0 ? resident : 1);
+    const int64_t waves = cdiv64(ntile, slot_count);
+    const int64_t wave_cap = waves * slot_count;
+
+    // ---- clusters ----
+    const int64_t clusters = cdiv64(M, cm * tm) * cdiv64(N, cn * tn);
+    const int64_t cslots = max64(h.n_sm / (cm * cn), 1);
+    const int64_t cwaves = cdiv64(clusters, cslots);
+
+    // ---- bytes ----
+    const int64_t a_bytes = eb * M * K, b_bytes = eb * K * N;
+    const int64_t epi_traffic = 2 * ob * M * N;        // D written + C read
+    const int64_t loads = gn * a_bytes + gm * b_bytes; // every tile loads its panels
+    const int64_t conv = out_dtype != dtype ? M * N * ob : 0;
+    const int64_t gemm_flops = 2 * M * N * K;
+    const int64_t tile_flops = 2 * tm * tn * tk;
+
+    // ---- tier 1 ----
+    x[0] = lg(M); x[1] = lg(N); x[2] = lg(K); x[3] = lg(gemm_flops);
+    x[4] = exact(tm); x[5] = exact(tn); x[6] = exact(tk); x[7] = exact(st);
+    x[8] = exact(cm); x[9] = exact(cn); x[10] = exact(cm * cn); x[11] = exact(swz);
+    x[12] = exact(gm); x[13] = exact(gn); x[14] = exact(gk); x[15] = exact(ntile);
+    x[16] = quot(gm * tm - M, M);
+    x[17] = quot(gn * tn - N, N);
+    x[18] = quot(gk * tk - K, K);
+    x[19] = quot(ntile, h.n_sm);
+    x[20] = exact(threads);
+    x[21] = quot(tm * tn, threads);
+    x[22] = exact(regs);
+    x[23] = exact(by_regs);
+    x[24] = exact(stage_bytes);
+    x[25] = exact(main_bytes);
+    x[26] = exact(epi_bytes);
+    x[27] = exact(smem);
+    x[28] = quot(smem, h.smem_sm);
+    x[29] = exact(by_smem);
+    x[30] = exact(by_arch);
+    x[31] = exact(resident);
+    x[32] = exact(fits ? 1 : 0);
+    x[33] = exact(waves);
+    x[34] = quot(ntile, wave_cap);
+    x[35] = quot(wave_cap - ntile, wave_cap);
+    x[36] = exact(clusters);
+    x[37] = exact(cslots);
+    x[38] = exact(cwaves);
+    x[39] = quot(clusters, cwaves * cslots);
+    x[40] = quot(gm, cm);
+    x[41] = quot(gn, cn);
+    x[42] = exact((cm > gm || cn > gn) ? 1 : 0);
+    x[43] = quot(gemm_flops, a_bytes + b_bytes + epi_traffic);
+    x[44] = quot(2 * tm * tn, (tm + tn) * eb);
+    x[45] = quot(loads, a_bytes + b_bytes);
+    x[46] = quot(a_bytes + b_bytes, h.llc);
+    x[47] = quot((tm + tn) * K * eb, h.llc);
+    x[48] = exact(loads);
+    x[49] = exact(epi_traffic);
+    const double t_load = (double)(h.n_sm * stage_bytes) / (double)h.bw;
+    const double t_mma = (double)(tile_flops * h.n_sm) / (double)(consumers * pk);
+    x[50] = quot(h.n_sm * stage_bytes, h.bw);
+    x[51] = quot(tile_flops * h.n_sm, consumers * pk);
+    x[52] = quot(tile_flops * h.bw, consumers * pk * stage_bytes);
+    x[53] = quot(min64(st, gk), st);
+    x[54] = quot(gk, st);
+    x[55] = quot(st * smem, h.smem_sm);
+    x[56] = exact(tk * st);
+    x[57] = exact(st * resident);
+    {
+        const double fill = (double)(clusters * st) / (double)(cwaves * cslots * cm * cn);
+        x[58] = (float)(fill * sqrt((double)(tm * tn * tk)));
+    }
+    x[59] = exact(h.n_sm); x[60] = exact(h.smem_sm); x[61] = exact(h.regs_sm);
+    x[62] = exact(h.llc); x[63] = exact(h.bw);
+
+    const bool a_colmajor = layout == lNN || layout == lNT;
+    const bool b_rowmajor = layout == lTT || layout == lNT;
+    const bool streamk = ts == tStreamK;
+    const double stage_t = t_load > t_mma ? t_load : t_mma;
+
+    if constexpr (F > 64) {
+        x[64] = exact(layout); x[65] = exact(a_colmajor); x[66] = exact(b_rowmajor);
+        x[67] = exact(dtype); x[68] = exact(dFp32); x[69] = exact(out_dtype);
+        x[70] = exact(eb); x[71] = exact(eb); x[72] = exact(ob);
+        x[73] = exact(ks); x[74] = exact(es); x[75] = exact(ts); x[76] = exact(streamk);
+        x[77] = exact(consumers); x[78] = exact(h.arch_id); x[79] = exact(pk);
+        x[80] = quot(pk, h.bw);
+        x[81] = (float)(((double)gemm_flops / (double)(a_bytes + b_bytes + epi_traffic)) /
+                        ((double)pk / (double)h.bw));
+        const bool ok_a = !a_colmajor || tk <= 256 * cn;
+        const bool ok_b = !b_rowmajor || tk <= 256 * cm;
+        const bool ok_coop = ks != kCoop || (tm % 128) == 0;
+        const bool ok_sk = !streamk || ks == kCoop;
+        x[82] = exact(ok_a); x[83] = exact(ok_b); x[84] = exact(ok_coop); x[85] = exact(ok_sk);
+        x[86] = exact(tn <= 2 * M && tn <= 2 * N);
+        x[87] = exact(fits && ok_a && ok_b && ok_coop && ok_sk);
+        x[88] = exact(conv);
+        const int64_t traffic = loads + epi_traffic + conv;
+        x[89] = exact(traffic);
+        x[90] = quot(traffic, h.bw);
+        const int64_t padded = (gm * tm) * (gn * tn) * (gk * tk);
+        x[91] = quot(2 * padded, pk);
+        x[92] = quot(padded, M * N * K);
+        x[93] = exact(h.smem_block - smem);
+        x[94] = exact(by_smem == resident);
+        x[95] = exact(by_regs == resident);
+    }
+    if constexpr (F > 96) {
+        const int64_t per_kblock = cdiv64(tm, im) * cdiv64(tn, in_) * cdiv64(tk, ik);
+        x[96] = exact(im); x[97] = exact(in_); x[98] = exact(ik);
+        x[99] = exact(per_kblock); x[100] = exact(per_kblock * gk);
+        x[101] = exact(cdiv64(tm, 64)); x[102] = exact(tm * tn); x[103] = exact(tm * tn * tk);
+        x[104] = (float)sqrt((double)(tm * tn * tk));
+        x[105] = exact(tm * K * eb); x[106] = exact(tn * K * eb);
+        x[107] = exact(tm * tn * ob); x[108] = exact(4 * tm * tn);
+        x[109] = exact(min64(st, gk)); x[110] = exact(max64(gk - st, 0));
+        const double mainloop_t = stage_t * (double)gk;
+        x[111] = (float)stage_t;
+        x[112] = (float)mainloop_t;
+        x[113] = (float)(mainloop_t * (double)waves);
+        x[114] = exact(streamk ? ntile * gk : 0);
+        x[115] = streamk ? x[35] : 0.0f;
+        x[116] = exact(resident * threads);
+        x[117] = quot(resident * threads, h.threads_sm_max);
+        x[118] = exact(by_arch == resident);
+        x[119] = quot(a_bytes, h.llc);
+        x[120] = quot(b_bytes, h.llc);
+        x[121] = quot(ob * M * N, h.llc);
+        x[122] = quot(M, N);
+        x[123] = quot(K, max64(M, N));
+        x[124] = quot(clusters, cslots);
+        const int64_t edge = ntile - (M / tm) * (N / tn);
+        x[125] = exact(edge);
+        x[126] = quot(edge, ntile);
+        x[127] = lg(ntile);
+    }
+}
+
+constexpr int kWaves = 4;
+
+template <int F>
+__global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_problem_t *__restrict__ probs,
+                                                          int32_t P, const int64_t *__restrict__ seg,
+                                                          CandsDev c, int64_t R, float *__restrict__ X,
+                                                          int64_t ld)
+{
+    __shared__ float stage[kWaves][64][33];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t row0 = ((int64_t)blockIdx.x * kWaves + wave) * 64;
+    const int64_t r = row0 + lane;
+    float x[F];
+    if (r < R) {
+        const int32_t p = segment_of_row(seg, P, r);
+        const hwsel_problem_t pb = probs[p];
+        phi<F>(h, pb, c, r, x);
+    } else {
+#pragma unroll
+        for (int j = 0; j < F; ++j) x[j] = 0.0f;
+    }
+#pragma unroll
+    for (int ch = 0; ch < F / 32; ++ch) {
+#pragma unroll
+        for (int j = 0; j < 32; ++j) stage[wave][lane][j] = x[ch * 32 + j];
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int q = lane + 64 * i;
+            const int rr = q >> 3, cc = (q & 7) * 4;
+            const int64_t gr = row0 + rr;
+            if (gr < R) {
+                const float4 v = make_float4(stage[wave][rr][cc], stage[wave][rr][cc + 1],
+                                             stage[wave][rr][cc + 2], stage[wave][rr][cc + 3]);
+                *reinterpret_cast<float4 *>(X + gr * ld + ch * 32 + cc) = v;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+hipError_t launch_features(const HwDev &hw, const hwsel_problem_t *problems, int32_t P,
+                           const int64_t *seg, const CandsDev &c, int64_t R, int32_t F, float *X,
+                           int64_t ld, hipStream_t s)
+{
+    const int64_t rows_per_block = 64 * kWaves;
+    const dim3 grid((unsigned)((R + rows_per_block - 1) / rows_per_block));
+    const dim3 block(64 * kWaves);
+    if (F == 64)
+        hipLaunchKernelGGL(k_features<64>, grid, block, 0, s, hw, problems, P, seg, c, R, X, ld);
+    else if (F == 96)
+        hipLaunchKernelGGL(k_features<96>, grid, block, 0, s, hw, problems, P, seg, c, R, X, ld);
+    else
+        hipLaunchKernelGGL(k_features<128>, grid, block, 0, s, hw, problems, P, seg, c, R, X, ld);
+    return hipGetLastError();
+}
+
+}  // namespace hwsel

@@ -1,0 +1,59 @@
+// Internal launch interface between the C-ABI layer (api.hip) and the kernel
+// translation units.  Launchers assume their arguments were checked by the
+// caller and only enqueue work.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/hwsel.h"
+
+namespace hwsel {
+
+// Hardware descriptor as the kernels read it (plain copy of hwsel_hw_t).
+struct HwDev {
+    int64_t n_sm, smem_sm, smem_block, smem_rsv;
+    int64_t regs_sm, regs_thread_max, blocks_sm_max, threads_sm_max;
+    int64_t arch_id, llc, bw;
+    int64_t peak[3];
+};
+
+struct CandsDev {
+    const uint16_t *tile_m, *tile_n, *tile_k, *inst_n;
+    const uint8_t *stages, *cluster_m, *cluster_n, *swizzle, *inst_m_div16, *inst_k;
+    const uint8_t *kernel_sched, *epi_sched, *tile_sched;
+};
+
+hipError_t launch_features(const HwDev &hw, const hwsel_problem_t *problems, int32_t P,
+                           const int64_t *seg, const CandsDev &c, int64_t R, int32_t F, float *X,
+                           int64_t ld, hipStream_t s);
+
+hipError_t launch_forest_score(const hwsel_forest_t &f, const float *X, int64_t R, int64_t ld,
+                               float *scores, hipStream_t s);
+
+hipError_t launch_forest_leaves(const hwsel_forest_t &f, const float *X, int64_t R, int64_t ld,
+                                const int64_t *rows, int64_t n_rows, uint16_t *leaf_idx,
+                                hipStream_t s);
+
+hipError_t launch_mlp(const hwsel_mlp_t &m, const float *X, int64_t R, int64_t ld, float *scores,
+                      hipStream_t s);
+
+hipError_t launch_topk(const float *scores, const int64_t *seg, int32_t P, int32_t k, int32_t *idx,
+                       float *vals, hipStream_t s);
+
+hipError_t launch_regret(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx,
+                         int32_t k, float *r1, float *rk, int32_t *best, hipStream_t s);
+
+// Last segment p with seg[p] <= r (segments are [seg[p], seg[p+1])); the
+// result is always in [0, P-1], whatever the offsets hold.
+__device__ inline int32_t segment_of_row(const int64_t *__restrict__ seg, int32_t P, int64_t r)
+{
+    int32_t lo = 0, hi = P;
+    while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (seg[mid] <= r) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+}  // namespace hwsel

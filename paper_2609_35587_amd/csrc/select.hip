@@ -1,0 +1,171 @@
+// Per-problem selection (top-k by score) and selection regret.
+//
+// One workgroup per problem segment.  Scores are mapped to 64-bit keys
+// (order-preserving score bits << 32 | inverted local index), which makes
+// every key unique: "score descending, index ascending" becomes "key
+// descending" and the answer is unique.  The k best keys are found by k
+// rounds of a block-wide maximum restricted to keys below the previous
+// winner; a segment is read k times, from L2 after the first round.
+#include "internal.hpp"
+
+namespace hwsel {
+namespace {
+
+constexpr int kThreads = 256;
+
+// Larger key = better score.  NaN ranks lowest, -0 equals +0.
+__device__ __forceinline__ uint32_t desc_bits(float s)
+{
+    if (s != s) return 0u;
+    uint32_t b = __float_as_uint(s);
+    if ((b << 1) == 0u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Smaller key = faster runtime.  NaN ranks above +inf, -0 equals +0.
+__device__ __forceinline__ uint32_t asc_bits(float t)
+{
+    if (t != t) return 0xffffffffu;
+    uint32_t b = __float_as_uint(t);
+    if ((b << 1) == 0u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t wave_max(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t w = __shfl_xor(v, o, 64);
+        v = w > v ? w : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_min(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t w = __shfl_xor(v, o, 64);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+
+template <bool kMax>
+__device__ uint64_t block_reduce(uint64_t v, uint64_t *sh)
+{
+    v = kMax ? wave_max(v) : wave_min(v);
+    const int wave = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) sh[wave] = v;
+    __syncthreads();
+    uint64_t r = sh[0];
+#pragma unroll
+    for (int w = 1; w < kThreads / 64; ++w) r = kMax ? (sh[w] > r ? sh[w] : r) : (sh[w] < r ? sh[w] : r);
+    return r;
+}
+
+__device__ __forceinline__ int64_t seg_len(const int64_t *seg, int32_t p)
+{
+    int64_t n = seg[p + 1] - seg[p];
+    n = n < 0 ? 0 : n;
+    return n > 0x7fffffff ? 0x7fffffff : n;
+}
+
+__global__ __launch_bounds__(kThreads) void k_topk(const float *__restrict__ scores,
+                                                    const int64_t *__restrict__ seg, int32_t k,
+                                                    int32_t *__restrict__ idx, float *__restrict__ vals)
+{
+    __shared__ uint64_t sh[kThreads / 64];
+    const int32_t p = blockIdx.x;
+    const int64_t base = seg[p];
+    const int64_t n = seg_len(seg, p);
+    const float *s = scores + base;
+    uint64_t prev = ~0ull;
+    for (int32_t j = 0; j < k; ++j) {
+        uint64_t best = 0;
+        for (int64_t i = threadIdx.x; i < n; i += kThreads) {
+            const uint64_t key = ((uint64_t)desc_bits(s[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
+            best = (key < prev && key > best) ? key : best;
+        }
+        best = block_reduce<true>(best, sh);
+        if (threadIdx.x == 0) {
+            const int64_t o = (int64_t)p * k + j;
+            if (best == 0) {
+                idx[o] = -1;
+                if (vals) vals[o] = -__builtin_inff();
+            } else {
+                const int32_t li = (int32_t)(0xffffffffu - (uint32_t)best);
+                idx[o] = li;
+                if (vals) vals[o] = s[li];
+            }
+        }
+        prev = best;
+    }
+}
+
+__device__ __forceinline__ float regret_value(float t_star, float t_pick)
+{
+    if (t_pick == t_star) return 0.0f;
+    return (float)(1.0 - (double)t_star / (double)t_pick);
+}
+
+__global__ __launch_bounds__(kThreads) void k_regret(const float *__restrict__ rt,
+                                                      const int64_t *__restrict__ seg,
+                                                      const int32_t *__restrict__ idx, int32_t k,
+                                                      float *__restrict__ r1, float *__restrict__ rk,
+                                                      int32_t *__restrict__ best)
+{
+    __shared__ uint64_t sh[kThreads / 64];
+    const int32_t p = blockIdx.x;
+    const int64_t base = seg[p];
+    const int64_t n = seg_len(seg, p);
+    const float *t = rt + base;
+    uint64_t m = ~0ull;
+    for (int64_t i = threadIdx.x; i < n; i += kThreads) {
+        const uint64_t key = ((uint64_t)asc_bits(t[i]) << 32) | (uint64_t)(uint32_t)i;
+        m = key < m ? key : m;
+    }
+    m = block_reduce<false>(m, sh);
+    if (threadIdx.x != 0) return;
+    if (n == 0) {
+        r1[p] = __builtin_nanf("");
+        if (rk) rk[p] = __builtin_nanf("");
+        if (best) best[p] = -1;
+        return;
+    }
+    const int32_t b = (int32_t)(uint32_t)m;
+    const float t_star = t[b];
+    const int32_t *pick = idx + (int64_t)p * k;
+    const int32_t c0 = pick[0];
+    r1[p] = (c0 >= 0 && c0 < n) ? regret_value(t_star, t[c0]) : __builtin_nanf("");
+    if (rk) {
+        uint64_t bk = ~0ull;
+        for (int32_t j = 0; j < k; ++j) {
+            const int32_t c = pick[j];
+            if (c < 0 || c >= n) continue;
+            const uint64_t key = ((uint64_t)asc_bits(t[c]) << 32) | (uint64_t)(uint32_t)c;
+            bk = key < bk ? key : bk;
+        }
+        rk[p] = bk == ~0ull ? __builtin_nanf("") : regret_value(t_star, t[(uint32_t)bk]);
+    }
+    if (best) best[p] = b;
+}
+
+}  // namespace
+
+hipError_t launch_topk(const float *scores, const int64_t *seg, int32_t P, int32_t k, int32_t *idx,
+                       float *vals, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_topk, dim3(P), dim3(kThreads), 0, s, scores, seg, k, idx, vals);
+    return hipGetLastError();
+}
+
+hipError_t launch_regret(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx,
+                         int32_t k, float *r1, float *rk, int32_t *best, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_regret, dim3(P), dim3(kThreads), 0, s, rt, seg, idx, k, r1, rk, best);
+    return hipGetLastError();
+}
+
+}  // namespace hwsel

@@ -1,0 +1,226 @@
+"""Python binding of libhwsel.so (ctypes).
+
+The functions carry the C ABI's names and only marshal arguments: torch
+tensors in device memory become raw pointers, the current torch stream
+becomes the hipStream_t.  Every step of the scored path runs in the HIP
+library; there is no fallback of any kind -- if the library is missing the
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhwsel.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "hwsel.h")
+
+HWSEL_OK, HWSEL_EINVAL, HWSEL_EUNSUPPORTED, HWSEL_EHIP = 0, 1, 2, 3
+
+
+class HwselError(RuntimeError):
+    def __init__(self, fn: str, status: int, detail: str):
+        super().__init__(f"{fn} -> {status} ({detail})")
+        self.status = status
+
+
+class hwsel_hw_t(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in (
+        "n_sm", "smem_per_sm", "smem_per_block_max", "smem_reserved", "regs_per_sm",
+        "max_regs_per_thread", "max_blocks_per_sm", "max_threads_per_sm", "arch_id",
+        "llc_bytes", "hbm_bw_gbps")] + [("peak_gflops", C.c_int64 * 3)]
+
+
+CAND_FIELDS = ("tile_m", "tile_n", "tile_k", "inst_n", "stages", "cluster_m", "cluster_n", "swizzle",
+               "inst_m_div16", "inst_k", "kernel_sched", "epi_sched", "tile_sched")
+
+
+class hwsel_cands_t(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in CAND_FIELDS]
+
+
+class hwsel_forest_t(C.Structure):
+    _fields_ = [("n_trees", C.c_int32), ("depth", C.c_int32), ("n_features", C.c_int32),
+                ("flags", C.c_uint32), ("base_score", C.c_float), ("node_feature", C.c_void_p),
+                ("node_threshold", C.c_void_p), ("leaf_value", C.c_void_p)]
+
+
+class hwsel_mlp_t(C.Structure):
+    _fields_ = [("n_in", C.c_int32), ("h1", C.c_int32), ("h2", C.c_int32), ("h3", C.c_int32),
+                ("mean", C.c_void_p), ("inv_std", C.c_void_p), ("W1", C.c_void_p), ("W2", C.c_void_p),
+                ("W3", C.c_void_p), ("W4", C.c_void_p), ("b1", C.c_void_p), ("b2", C.c_void_p),
+                ("b3", C.c_void_p), ("b4", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load the HIP library; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python paper_2609_35587_amd/build.py` (there is no CPU fallback)")
+        L = C.CDLL(LIB_PATH)
+        L.hwsel_status_string.restype = C.c_char_p
+        L.hwsel_last_error.restype = C.c_char_p
+        vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
+        L.hwsel_features.argtypes = [hwsel_hw_t, vp, i32, vp, C.POINTER(hwsel_cands_t), i64, i32, vp, i64, vp]
+        L.hwsel_forest_score.argtypes = [C.POINTER(hwsel_forest_t), vp, i64, i64, vp, vp]
+        L.hwsel_forest_leaves.argtypes = [C.POINTER(hwsel_forest_t), vp, i64, i64, vp, i64, vp, vp]
+        L.hwsel_mlp_score.argtypes = [C.POINTER(hwsel_mlp_t), vp, i64, i64, vp, vp]
+        L.hwsel_topk_per_problem.argtypes = [vp, vp, i32, i32, vp, vp, vp]
+        L.hwsel_regret.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, status: int) -> None:
+    if status != HWSEL_OK:
+        raise HwselError(fn, status, lib().hwsel_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dev(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    return t
+
+
+# ----------------------------------------------------------------------------
+# Marshalling helpers (numpy -> device tensors); no arithmetic of the path.
+# ----------------------------------------------------------------------------
+def to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    elif a.dtype.fields is not None:
+        a = a.view(np.uint8).reshape(len(a), -1)
+    return torch.from_numpy(a).to(device)
+
+
+def hw_struct(hw: dict) -> hwsel_hw_t:
+    s = hwsel_hw_t()
+    for n, _ in hwsel_hw_t._fields_[:-1]:
+        setattr(s, n, int(hw[n]))
+    for i, v in enumerate(hw["peak_gflops"]):
+        s.peak_gflops[i] = int(v)
+    return s
+
+
+# ----------------------------------------------------------------------------
+# Entry points
+# ----------------------------------------------------------------------------
+def hwsel_features(hw: dict, problems: torch.Tensor, seg_offsets: torch.Tensor, cands: dict,
+                   n_features: int, X: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """problems: uint8 [P, 16] device records; seg_offsets int64 [P+1];
+    cands: name -> device tensor of length R.  Returns X fp32 [R, ld]."""
+    P = problems.shape[0]
+    R = cands["tile_m"].shape[0]
+    if X is None:
+        X = torch.empty((R, n_features), dtype=torch.float32, device=problems.device)
+    cs = hwsel_cands_t(*[_ptr(_dev(cands[n], n)) for n in CAND_FIELDS])
+    _check("hwsel_features", lib().hwsel_features(
+        hw_struct(hw), _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")),
+        C.byref(cs), R, n_features, _ptr(X), X.stride(0), _stream(stream)))
+    return X
+
+
+def forest_struct(f: dict) -> hwsel_forest_t:
+    return hwsel_forest_t(int(f["n_trees"]), int(f["depth"]), int(f["n_features"]), int(f["flags"]),
+                          float(f["base_score"]), _ptr(f["node_feature"]), _ptr(f["node_threshold"]),
+                          _ptr(f["leaf_value"]))
+
+
+def hwsel_forest_score(forest: dict, X: torch.Tensor, scores: torch.Tensor | None = None,
+                       stream=None) -> torch.Tensor:
+    R = X.shape[0]
+    if scores is None:
+        scores = torch.empty(R, dtype=torch.float32, device=X.device)
+    s = forest_struct(forest)
+    _check("hwsel_forest_score", lib().hwsel_forest_score(
+        C.byref(s), _ptr(X), R, X.stride(0), _ptr(scores), _stream(stream)))
+    return scores
+
+
+def hwsel_forest_leaves(forest: dict, X: torch.Tensor, rows: torch.Tensor,
+                        leaf_idx: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    n = rows.shape[0]
+    if leaf_idx is None:
+        leaf_idx = torch.empty((n, int(forest["n_trees"])), dtype=torch.int16, device=X.device)
+    s = forest_struct(forest)
+    _check("hwsel_forest_leaves", lib().hwsel_forest_leaves(
+        C.byref(s), _ptr(X), X.shape[0], X.stride(0), _ptr(_dev(rows, "rows")), n, _ptr(leaf_idx),
+        _stream(stream)))
+    return leaf_idx
+
+
+def mlp_struct(m: dict) -> hwsel_mlp_t:
+    return hwsel_mlp_t(128, 512, 512, 256, *[_ptr(m[n]) for n in
+                                             ("mean", "inv_std", "W1", "W2", "W3", "W4", "b1", "b2", "b3", "b4")])
+
+
+def hwsel_mlp_score(mlp: dict, X: torch.Tensor, scores: torch.Tensor | None = None,
+                    stream=None) -> torch.Tensor:
+    R = X.shape[0]
+    if scores is None:
+        scores = torch.empty(R, dtype=torch.float32, device=X.device)
+    s = mlp_struct(mlp)
+    _check("hwsel_mlp_score", lib().hwsel_mlp_score(C.byref(s), _ptr(X), R, X.stride(0), _ptr(scores),
+                                                    _stream(stream)))
+    return scores
+
+
+def hwsel_topk_per_problem(scores: torch.Tensor, seg_offsets: torch.Tensor, k: int,
+                           idx: torch.Tensor | None = None, vals: torch.Tensor | None = None,
+                           with_vals: bool = True, stream=None):
+    P = seg_offsets.shape[0] - 1
+    if idx is None:
+        idx = torch.empty((P, k), dtype=torch.int32, device=scores.device)
+    if vals is None and with_vals:
+        vals = torch.empty((P, k), dtype=torch.float32, device=scores.device)
+    _check("hwsel_topk_per_problem", lib().hwsel_topk_per_problem(
+        _ptr(_dev(scores, "scores")), _ptr(_dev(seg_offsets, "seg_offsets")), P, k, _ptr(idx), _ptr(vals),
+        _stream(stream)))
+    return idx, vals
+
+
+def hwsel_regret(runtimes: torch.Tensor, seg_offsets: torch.Tensor, idx: torch.Tensor,
+                 r1: torch.Tensor | None = None, rk: torch.Tensor | None = None,
+                 best: torch.Tensor | None = None, stream=None):
+    P, k = idx.shape
+    dev = runtimes.device
+    r1 = torch.empty(P, dtype=torch.float32, device=dev) if r1 is None else r1
+    rk = torch.empty(P, dtype=torch.float32, device=dev) if rk is None else rk
+    best = torch.empty(P, dtype=torch.int32, device=dev) if best is None else best
+    _check("hwsel_regret", lib().hwsel_regret(
+        _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P, _ptr(_dev(idx, "idx")), k,
+        _ptr(r1), _ptr(rk), _ptr(best), _stream(stream)))
+    return r1, rk, best
+
+
+def declared_functions() -> list[str]:
+    """Names of the functions include/hwsel.h declares."""
+    import re
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hwsel_[a-z0-9_]+)\s*\(", text)))

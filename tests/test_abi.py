@@ -1,0 +1,101 @@
+"""The C-ABI library loads on a machine without a GPU, exports every function
+include/hwsel.h declares, and rejects bad arguments on the host before any
+HIP call (so these run without a GPU)."""
+import ctypes as C
+import os
+import subprocess
+
+import pytest
+
+from paper_2609_35587_amd import hwsel
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(hwsel.LIB_PATH):
+        pytest.fail("libhwsel.so is not built (python paper_2609_35587_amd/build.py)")
+    return hwsel.lib()
+
+
+def test_exports_every_declared_function(L):
+    names = hwsel.declared_functions()
+    assert len(names) >= 8
+    out = subprocess.run(["nm", "-D", "--defined-only", hwsel.LIB_PATH], capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+
+
+def test_status_strings(L):
+    assert L.hwsel_status_string(0) == b"ok"
+    assert L.hwsel_status_string(1) == b"invalid argument"
+    assert L.hwsel_status_string(99) == b"unknown status"
+
+
+FAKE = 0x1000   # never dereferenced: every call below is rejected first
+
+
+def _cands(**null):
+    vals = [None if n in null else FAKE for n in hwsel.CAND_FIELDS]
+    return hwsel.hwsel_cands_t(*vals)
+
+
+def _hw(**over):
+    hw = dict(n_sm=132, smem_per_sm=233472, smem_per_block_max=232448, smem_reserved=2048, regs_per_sm=65536,
+              max_regs_per_thread=255, max_blocks_per_sm=32, max_threads_per_sm=2048, arch_id=90,
+              llc_bytes=52428800, hbm_bw_gbps=4000, peak_gflops=(989500, 989500, 1979000))
+    hw.update(over)
+    return hwsel.hw_struct(hw)
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(problems=None), 1), (dict(cands=_cands(stages=1)), 1), (dict(P=0), 1), (dict(R=0), 1),
+    (dict(F=100), 2), (dict(ld=130), 1), (dict(ld=64), 1), (dict(X=FAKE + 4), 1),
+    (dict(hw=_hw(n_sm=0)), 1), (dict(hw=_hw(smem_reserved=-1)), 1), (dict(hw=_hw(peak_gflops=(1, 0, 1))), 1),
+])
+def test_features_rejects(L, case, status):
+    a = dict(hw=_hw(), problems=FAKE, P=4, seg=FAKE, cands=_cands(), R=100, F=128, X=FAKE, ld=128)
+    a.update(case)
+    rc = L.hwsel_features(a["hw"], a["problems"], a["P"], a["seg"], C.byref(a["cands"]), a["R"], a["F"], a["X"],
+                          a["ld"], None)
+    assert rc == status
+    assert L.hwsel_last_error().startswith(b"hwsel_features: ")
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(depth=0), 2), (dict(depth=13), 2), (dict(n_trees=0), 1), (dict(n_features=0), 2),
+    (dict(n_features=300), 2), (dict(node_feature=None), 1), (dict(ld=3), 1), (dict(R=0), 1),
+])
+def test_forest_rejects(L, over, status):
+    f = dict(n_trees=10, depth=6, n_features=64, flags=1, base_score=0.0, node_feature=FAKE,
+             node_threshold=FAKE, leaf_value=FAKE)
+    ld = over.pop("ld", 64)
+    R = over.pop("R", 100)
+    f.update(over)
+    s = hwsel.forest_struct(f)
+    assert L.hwsel_forest_score(C.byref(s), FAKE, R, ld, FAKE, None) == status
+    assert L.hwsel_forest_leaves(C.byref(s), FAKE, R, ld, FAKE, 5, FAKE, None) == status
+
+
+def test_forest_leaves_rejects_empty_row_list(L):
+    f = dict(n_trees=10, depth=6, n_features=64, flags=1, base_score=0.0, node_feature=FAKE,
+             node_threshold=FAKE, leaf_value=FAKE)
+    assert L.hwsel_forest_leaves(C.byref(hwsel.forest_struct(f)), FAKE, 100, 64, FAKE, 0, FAKE, None) == 1
+
+
+def test_mlp_rejects(L):
+    m = hwsel.hwsel_mlp_t(128, 512, 512, 256, *([FAKE] * 10))
+    assert L.hwsel_mlp_score(C.byref(m), FAKE, 0, 128, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m), FAKE, 10, 100, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m), FAKE + 8, 10, 128, FAKE, None) == 1
+    m2 = hwsel.hwsel_mlp_t(128, 256, 512, 256, *([FAKE] * 10))
+    assert L.hwsel_mlp_score(C.byref(m2), FAKE, 10, 128, FAKE, None) == 2
+    m3 = hwsel.hwsel_mlp_t(128, 512, 512, 256, *([FAKE] * 9), None)
+    assert L.hwsel_mlp_score(C.byref(m3), FAKE, 10, 128, FAKE, None) == 1
+
+
+@pytest.mark.parametrize("P,k,status", [(0, 5, 1), (4, 0, 1), (4, 65, 1)])
+def test_select_rejects(L, P, k, status):
+    assert L.hwsel_topk_per_problem(FAKE, FAKE, P, k, FAKE, None, None) == status
+    assert L.hwsel_regret(FAKE, FAKE, P, FAKE, k, FAKE, None, None, None) == status
+    assert L.hwsel_regret(None, FAKE, 4, FAKE, 5, FAKE, None, None, None) == 1

@@ -1,0 +1,175 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Small workloads are compared on every row; the large ones run at full size
+in the launch configuration the benchmark times and are compared on a seeded
+row sample the oracle evaluates one by one, plus properties that hold at any
+size.  Acceptance:
+  features  - integer columns bit-exact, other columns within 1e-6 relative;
+  forest    - leaf indices bit-exact, scores within 1e-5 * max(|o|, L1 of the
+              row's leaf values);
+  MLP       - within 2e-2 * max(|o|, rms of the oracle scores);
+  top-k     - bit-exact indices on identical scores;
+  regret    - bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from _gpu_util import Dev, assert_forest_scores, compare_features, path_l1, say
+from paper_2609_35587_amd import hwsel
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE = 65536
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    w = synth.workload("tiny")
+    return w, Dev(w)
+
+
+# ----------------------------------------------------------------------------
+# tiny: every row, every stage, plus the end-to-end selection
+# ----------------------------------------------------------------------------
+def test_features_tiny_all_rows(tiny):
+    w, d = tiny
+    say("features tiny")
+    X = d.features(64).cpu().numpy()
+    ref = oracle.features(w.hw, w.problems, w.seg, w.cands, 64)
+    say(f"  {compare_features(X, ref, 64)}")
+
+
+def test_forest_tiny_all_rows(tiny):
+    w, d = tiny
+    say("forest tiny")
+    ref_X = oracle.features(w.hw, w.problems, w.seg, w.cands, 64)
+    Xd = torch.from_numpy(ref_X).cuda()             # identical input on both sides
+    s = hwsel.hwsel_forest_score(d.forest, Xd).cpu().numpy()
+    rows = torch.arange(len(ref_X), dtype=torch.int64, device="cuda")
+    li = hwsel.hwsel_forest_leaves(d.forest, Xd, rows).cpu().numpy().view(np.uint16)
+    o, oli = oracle.forest(w.forest, ref_X, leaves=True)
+    assert np.array_equal(li, oli)
+    say(f"  score err/bound max {assert_forest_scores(s, o, path_l1(w.forest, oli)):.3g}")
+
+
+def test_selection_tiny_end_to_end(tiny):
+    w, d = tiny
+    say("pipeline tiny")
+    k = w.cfg.k
+    X = d.features(64)
+    s = hwsel.hwsel_forest_score(d.forest, X)
+    idx, vals = hwsel.hwsel_topk_per_problem(s, d.seg, k)
+    r1, rk, best = hwsel.hwsel_regret(d.runtimes, d.seg, idx)
+    torch.cuda.synchronize()
+    ref_X = oracle.features(w.hw, w.problems, w.seg, w.cands, 64)
+    o = oracle.forest(w.forest, ref_X)
+    oidx, ovals = oracle.topk(o, w.seg, k)
+    assert np.array_equal(idx.cpu().numpy(), oidx)
+    o1, ok, ob = oracle.regret(w.runtimes, w.seg, oidx)
+    assert np.array_equal(r1.cpu().numpy().view(np.uint32), o1.view(np.uint32))
+    assert np.array_equal(rk.cpu().numpy().view(np.uint32), ok.view(np.uint32))
+    assert np.array_equal(best.cpu().numpy(), ob)
+    say(f"  mean regret top1 {o1.mean():.4f} best-of-{k} {ok.mean():.4f}")
+
+
+# ----------------------------------------------------------------------------
+# top-k and regret: ragged and empty segments, ties, NaN, signed zeros, k range
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("k", [1, 5, 16, 64])
+def test_topk_regret_edge_cases(k):
+    say(f"topk/regret edge k={k}")
+    rng = np.random.default_rng(100 + k)
+    seg = synth.ragged_segments(rng, 300, 700, empty_frac=0.1)
+    seg[-1] = seg[-2]          # the last segment empty too
+    R = int(seg[-1])
+    s = synth.random_scores(rng, R, tie_frac=0.4, n_levels=3)
+    s[rng.random(R) < 0.02] = np.nan
+    s[rng.random(R) < 0.02] = -0.0
+    s[rng.random(R) < 0.02] = 0.0
+    s[rng.random(R) < 0.01] = -np.inf
+    s[rng.random(R) < 0.01] = np.inf
+    rt = np.exp(rng.standard_normal(R)).astype(np.float32)
+    rt[rng.random(R) < 0.03] = np.inf
+    rt[rng.random(R) < 0.2] = 1.0          # many equal runtimes
+    sd, segd, rtd = (torch.from_numpy(a).cuda() for a in (s, seg, rt))
+    idx, vals = hwsel.hwsel_topk_per_problem(sd, segd, k)
+    oidx, ovals = oracle.topk(s, seg, k)
+    assert np.array_equal(idx.cpu().numpy(), oidx)
+    assert np.array_equal(vals.cpu().numpy().view(np.uint32), ovals.view(np.uint32))
+    r1, rk, best = hwsel.hwsel_regret(rtd, segd, idx)
+    o1, ok, ob = oracle.regret(rt, seg, oidx)
+    assert np.array_equal(r1.cpu().numpy().view(np.uint32), o1.view(np.uint32))
+    assert np.array_equal(rk.cpu().numpy().view(np.uint32), ok.view(np.uint32))
+    assert np.array_equal(best.cpu().numpy(), ob)
+
+
+def test_topk_single_long_segment_and_all_ties():
+    say("topk long segment")
+    n = 65536 * 3 + 17
+    seg = np.array([0, n, n + 5], np.int64)
+    s = np.zeros(n + 5, np.float32)
+    s[12345] = 1.0
+    idx, _ = hwsel.hwsel_topk_per_problem(torch.from_numpy(s).cuda(), torch.from_numpy(seg).cuda(), 64)
+    oidx, _ = oracle.topk(s, seg, 64)
+    assert np.array_equal(idx.cpu().numpy(), oidx)
+    assert oidx[0, 0] == 12345 and oidx[0, 1:].tolist() == list(range(63))
+
+
+# ----------------------------------------------------------------------------
+# Full-size workloads: sampled rows + properties
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["medium", "full", "dataset"])
+def test_forest_workload_full_size(name):
+    say(f"workload {name}: generate")
+    w = synth.workload(name)
+    cfg = w.cfg
+    d = Dev(w)
+    say(f"workload {name}: features R={cfg.rows} F={cfg.n_features}")
+    X = d.features(cfg.n_features)
+    rows = synth.sample_rows(cfg, SAMPLE)
+    rows_d = torch.from_numpy(rows).cuda()
+    Xs = X.index_select(0, rows_d).cpu().numpy()
+    ref = oracle.features(w.hw, w.problems, w.seg, w.cands, cfg.n_features, rows)
+    say(f"  features {compare_features(Xs, ref, cfg.n_features)}")
+    say(f"workload {name}: forest {cfg.trees}x{cfg.depth}")
+    s = hwsel.hwsel_forest_score(d.forest, X)
+    li = hwsel.hwsel_forest_leaves(d.forest, X, rows_d).cpu().numpy().view(np.uint16)
+    o, oli = oracle.forest(w.forest, ref, leaves=True)
+    assert np.array_equal(li, oli)
+    g = s.index_select(0, rows_d).cpu().numpy()
+    say(f"  forest err/bound {assert_forest_scores(g, o, path_l1(w.forest, oli)):.3g}")
+    assert bool(torch.isfinite(s).all())
+    say(f"workload {name}: top-k / regret")
+    idx, vals = hwsel.hwsel_topk_per_problem(s, d.seg, cfg.k)
+    r1, rk, best = hwsel.hwsel_regret(d.runtimes, d.seg, idx)
+    s_host = s.cpu().numpy()
+    oidx, ovals = oracle.topk(s_host, w.seg, cfg.k)
+    assert np.array_equal(idx.cpu().numpy(), oidx)
+    o1, ok, ob = oracle.regret(w.runtimes, w.seg, oidx)
+    assert np.array_equal(r1.cpu().numpy().view(np.uint32), o1.view(np.uint32))
+    assert np.array_equal(rk.cpu().numpy().view(np.uint32), ok.view(np.uint32))
+    assert np.array_equal(best.cpu().numpy(), ob)
+    say(f"  mean regret top1 {np.nanmean(o1):.4f}")
+
+
+def test_mlp_dataset_rows():
+    say("mlp: features of the dataset-scale rows")
+    w = synth.workload("mlp")
+    d = Dev(w)
+    X = d.features(128)
+    rows = synth.sample_rows(w.cfg, 8192)
+    rows_d = torch.from_numpy(rows).cuda()
+    say("mlp: score all rows")
+    s = hwsel.hwsel_mlp_score(d.mlp, X)
+    g = s.index_select(0, rows_d).cpu().numpy()
+    Xs = X.index_select(0, rows_d).cpu().numpy()
+    o = oracle.mlp(w.mlp, Xs)
+    rms = float(np.sqrt(np.mean(o.astype(np.float64) ** 2)))
+    err = np.abs(g.astype(np.float64) - o)
+    bound = 2e-2 * np.maximum(np.abs(o), rms)
+    say(f"  max err/bound {float((err / bound).max()):.3g}  rms {rms:.3g}")
+    assert np.all(err <= bound)
+    assert bool(torch.isfinite(s).all())
