@@ -97,6 +97,9 @@ def main():
     for n in ("node_feature", "node_threshold", "leaf_value"):
         forest[n] = hwsel.to_device(w.forest[n], dev)
     mlp = {n: hwsel.to_device(v, dev) for n, v in mw.items()}
+    log("pack forest (once per model)")
+    packed = hwsel.hwsel_forest_pack(forest)
+    ws = torch.empty(hwsel.hwsel_forest_workspace_bytes(forest, R), dtype=torch.uint8, device=dev)
     X = torch.empty((R, F), dtype=torch.float32, device=dev)
     s_f = torch.empty(R, dtype=torch.float32, device=dev)
     s_m = torch.empty(R, dtype=torch.float32, device=dev)
@@ -114,7 +117,7 @@ def main():
         mark(0)
         hwsel.hwsel_features(w.hw, probs, seg, cands, F, X=X)
         mark(1)
-        hwsel.hwsel_forest_score(forest, X, scores=s_f)
+        hwsel.hwsel_forest_score(forest, X, scores=s_f, packed=packed, workspace=ws)
         mark(2)
         hwsel.hwsel_topk_per_problem(s_f, seg, k, idx=outs[0][0], vals=outs[0][1])
         mark(3)

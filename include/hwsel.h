@@ -136,15 +136,39 @@ typedef struct hwsel_forest {
 } hwsel_forest_t;
 
 /*
+ * Packing: a one-time conversion of a forest into the layout the fast scorer
+ * reads (per-feature sorted distinct thresholds, u8 threshold ranks, trees
+ * grouped into LDS-sized chunks, see the exact-binning identity in
+ * forest.hip).  hwsel_forest_pack reads the forest's device arrays, builds
+ * the image on the host and writes `bytes` = hwsel_forest_pack_bytes() bytes
+ * to `packed` (device, 16-byte aligned).  It synchronises `stream` (a model
+ * is packed once, at load time).  Returns HWSEL_EUNSUPPORTED when a feature
+ * has more than 255 distinct thresholds, depth > 10 or n_features > 128 (the
+ * unpacked path covers those), HWSEL_EINVAL for a node feature >=
+ * n_features or a NaN threshold.
+ */
+int hwsel_forest_pack_bytes(const hwsel_forest_t *f, size_t *bytes);
+int hwsel_forest_pack(const hwsel_forest_t *f, void *packed, size_t bytes, void *stream);
+
+/* Device workspace (bytes) hwsel_forest_score needs for a packed forest and
+ * R rows: u8 bins [R][n_features rounded up to 16] and one fp32 partial sum
+ * per tree chunk and row. */
+int hwsel_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *bytes);
+
+/*
  * scores[r] = f(X[r]) for r < R, accumulated in fp32 in a fixed order (the
  * same inputs give bit-identical scores from run to run).
  *   X: fp32 [R][ld], ld >= n_features, as written by hwsel_features.
+ *   packed: NULL for the direct tree walk, or the image hwsel_forest_pack
+ *     wrote for this very forest; then `workspace` must hold
+ *     hwsel_forest_workspace_bytes(f, R) bytes (device, 256-byte aligned).
  * Returns HWSEL_EINVAL for null pointers, R < 1, n_trees < 1, ld <
- * n_features; HWSEL_EUNSUPPORTED for depth outside [1, 12] or n_features
- * outside [1, 256].
+ * n_features, a short or misaligned workspace; HWSEL_EUNSUPPORTED for depth
+ * outside [1, 12] or n_features outside [1, 256] (and for a packed call on a
+ * forest hwsel_forest_pack does not accept).
  */
-int hwsel_forest_score(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld,
-                       float *scores, void *stream);
+int hwsel_forest_score(const hwsel_forest_t *f, const void *packed, const float *X, int64_t R, int64_t ld,
+                       float *scores, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Leaf index of every tree for selected rows: leaf_idx[i][t] = index in

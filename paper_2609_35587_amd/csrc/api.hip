@@ -93,13 +93,63 @@ static int check_forest(const hwsel_forest_t *f, const float *X, int64_t R, int6
     return HWSEL_OK;
 }
 
-int hwsel_forest_score(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld, float *scores,
-                       void *stream)
+int hwsel_forest_pack_bytes(const hwsel_forest_t *f, size_t *bytes)
+{
+    static const char *fn = "hwsel_forest_pack_bytes";
+    if (!f || !bytes) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (f->n_trees < 1) return fail(HWSEL_EINVAL, fn, "n_trees=%d", f->n_trees);
+    if (!hwsel::packable(*f))
+        return fail(HWSEL_EUNSUPPORTED, fn, "depth=%d n_features=%d (packed: depth <= 10, n_features <= 128)",
+                    f->depth, f->n_features);
+    *bytes = hwsel::packed_bytes(*f);
+    g_err[0] = 0;
+    return HWSEL_OK;
+}
+
+int hwsel_forest_pack(const hwsel_forest_t *f, void *packed, size_t bytes, void *stream)
+{
+    static const char *fn = "hwsel_forest_pack";
+    size_t need = 0;
+    if (int s = hwsel_forest_pack_bytes(f, &need)) return s;
+    if (!packed || !f->node_feature || !f->node_threshold || !f->leaf_value)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (f->n_features < 1 || f->depth < 1) return fail(HWSEL_EINVAL, fn, "empty forest shape");
+    if (bytes < need) return fail(HWSEL_EINVAL, fn, "bytes=%zu < %zu", bytes, need);
+    if (!aligned16(packed)) return fail(HWSEL_EINVAL, fn, "packed not 16-byte aligned");
+    switch (hwsel::pack_forest(*f, packed, (hipStream_t)stream)) {
+    case hwsel::PackStatus::ok: g_err[0] = 0; return HWSEL_OK;
+    case hwsel::PackStatus::bad_feature: return fail(HWSEL_EINVAL, fn, "node feature >= n_features");
+    case hwsel::PackStatus::nan_threshold: return fail(HWSEL_EINVAL, fn, "NaN threshold");
+    case hwsel::PackStatus::too_many_thresholds:
+        return fail(HWSEL_EUNSUPPORTED, fn, "a feature has more than 255 distinct thresholds");
+    default: return fail(HWSEL_EHIP, fn, "copy failed: %s", hipGetErrorString(hipGetLastError()));
+    }
+}
+
+int hwsel_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *bytes)
+{
+    static const char *fn = "hwsel_forest_workspace_bytes";
+    size_t dummy = 0;
+    if (int s = hwsel_forest_pack_bytes(f, &dummy)) return s;
+    if (R < 1) return fail(HWSEL_EINVAL, fn, "R=%lld", (long long)R);
+    *bytes = hwsel::packed_workspace_bytes(*f, R);
+    return HWSEL_OK;
+}
+
+int hwsel_forest_score(const hwsel_forest_t *f, const void *packed, const float *X, int64_t R, int64_t ld,
+                       float *scores, void *workspace, size_t workspace_bytes, void *stream)
 {
     static const char *fn = "hwsel_forest_score";
     if (int s = check_forest(f, X, R, ld, fn)) return s;
     if (!scores) return fail(HWSEL_EINVAL, fn, "null scores");
-    return launched(hwsel::launch_forest_score(*f, X, R, ld, scores, (hipStream_t)stream), fn);
+    if (!packed) return launched(hwsel::launch_forest_score(*f, X, R, ld, scores, (hipStream_t)stream), fn);
+    if (!hwsel::packable(*f)) return fail(HWSEL_EUNSUPPORTED, fn, "forest shape cannot be packed");
+    if (!aligned16(packed)) return fail(HWSEL_EINVAL, fn, "packed not 16-byte aligned");
+    const size_t need = hwsel::packed_workspace_bytes(*f, R);
+    if (!workspace || workspace_bytes < need)
+        return fail(HWSEL_EINVAL, fn, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(HWSEL_EINVAL, fn, "workspace not 256-byte aligned");
+    return launched(hwsel::launch_forest_packed(*f, packed, X, R, ld, scores, workspace, (hipStream_t)stream), fn);
 }
 
 int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld, const int64_t *rows,

@@ -1,15 +1,49 @@
 // Tree-ensemble scoring: s(x) = base + sum_t leaf_t(x).
 //
-// Generic traversal: one thread per row walks every tree from the root; node
-// records (feature byte, fp32 threshold) and leaves come from global memory
-// through the caches, the row's feature values are gathered from X.  The leaf
-// sum is accumulated in fp32 in tree order, so results are bit-identical from
-// run to run.
+// Two paths share the decision rule "left iff x < threshold (or NaN with
+// the default-left flag)":
+//
+// Generic path (no packed model): one thread per row walks every tree from
+// the root, reading node records and leaves through the caches and the row's
+// fp32 features from X.  Any forest the header admits runs here.
+//
+// Packed path (model packed once by hwsel_forest_pack):
+//   * Exact binning.  For feature f let U_f be the sorted distinct
+//     thresholds the forest uses (at most 255).  With
+//     b_f(x) = #{u in U_f : u <= x}, and a node testing x < U_f[j],
+//     x < U_f[j]  <=>  b_f(x) <= j,
+//     so the traversal compares u8 bins with u8 threshold ranks and gives the
+//     same path as the fp32 compares (NaN is binned to 0 when it goes left,
+//     255 when it goes right).  A pass writes the bins of every row once:
+//     128 bytes per row instead of 512.
+//   * Trees in LDS.  Trees are grouped into chunks of TC trees whose nodes
+//     (u16 code: feature | rank << 8, heap order, slot i of tree t at
+//     i*TC + t) and leaves (fp32, leaf l of tree t at l*TC + t) fill about
+//     96 KB of LDS.  Interleaving by tree puts the TC lanes of a wave that walk
+//     TC different trees on distinct banks.
+//   * Lanes.  A wave walks 64/TC rows x TC trees at a time; four such groups
+//     are in flight per wave to cover LDS latency.  For TC = 64 all lanes read
+//     the same row's bins, which lie on distinct banks (conflict-free).
+//   * Chunk-stationary, XCD-aware persistent grid.  Each workgroup owns one
+//     chunk for a whole row range and streams 256-row tiles of bins through
+//     LDS.  Workgroup b runs on XCD b % 8; the workgroups of one XCD cover the
+//     same rows with different chunks, in step, so a tile is fetched from HBM
+//     once per XCD and re-read from that XCD's L2.
+//   * Deterministic sums.  A chunk's per-row sum is a fixed butterfly over
+//     its TC lanes, written to a per-chunk partial row; a last pass adds
+//     base + partials in chunk order.
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
 #include "internal.hpp"
 
 namespace hwsel {
 namespace {
 
+// ---------------------------------------------------------------------------
+// Generic path
+// ---------------------------------------------------------------------------
 struct ForestDev {
     int32_t n_trees, depth, n_features;
     uint32_t nan_left;
@@ -19,7 +53,6 @@ struct ForestDev {
     const float *leaf;
 };
 
-// Leaf reached by row x in tree t (index in [0, 2^depth)).
 __device__ __forceinline__ int32_t walk(const ForestDev &f, const float *__restrict__ x, int32_t t)
 {
     const int64_t n_int = ((int64_t)1 << f.depth) - 1;
@@ -66,8 +99,205 @@ ForestDev to_dev(const hwsel_forest_t &f)
                      f.node_feature, f.node_threshold, f.leaf_value};
 }
 
+// ---------------------------------------------------------------------------
+// Packed path: layout
+// ---------------------------------------------------------------------------
+constexpr int kBinSlots = 256;        // thresholds per feature incl. padding
+constexpr int kBinStrideLds = 257;    // LDS row stride (floats) of the bin table
+constexpr int kTileRows = 256;        // rows of bins per LDS tile
+constexpr int kTileStride = 132;      // LDS bytes per bin row (33 dwords)
+constexpr int kWaves = 16;            // waves per traversal workgroup
+constexpr int kIlp = 4;               // row groups in flight per wave
+constexpr int kXcds = 8;
+constexpr int kSlotsPerXcd = 32;      // one workgroup per CU
+constexpr int kBinThreads = 1024;
+
+struct PackGeom {
+    int tc, n_chunks, slots, stride;      // trees per chunk, chunks, heap slots (2^D), bin row bytes
+    size_t thr_bytes, chunk_bytes, node_bytes, total;
+};
+
+// Trees per chunk: fill ~96 KB of LDS with nodes (2 B) and leaves (4 B).
+int trees_per_chunk(int depth)
+{
+    int tc = 64;
+    while (tc > 1 && (size_t)tc * ((size_t)6 << depth) > 96 * 1024) tc >>= 1;
+    return tc;
+}
+
+PackGeom geometry(const hwsel_forest_t &f)
+{
+    PackGeom g;
+    g.tc = trees_per_chunk(f.depth);
+    g.n_chunks = (f.n_trees + g.tc - 1) / g.tc;
+    g.slots = 1 << f.depth;
+    g.stride = (f.n_features + 15) / 16 * 16;
+    g.thr_bytes = (size_t)f.n_features * kBinSlots * sizeof(float);
+    g.node_bytes = (size_t)g.slots * g.tc * 2;
+    g.chunk_bytes = g.node_bytes + (size_t)g.slots * g.tc * 4;
+    g.total = 256 + g.thr_bytes + (size_t)g.n_chunks * g.chunk_bytes;
+    return g;
+}
+
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// ---------------------------------------------------------------------------
+// Packed path: kernels
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict__ X, int64_t R, int64_t ld,
+                                                         const float *__restrict__ U, int nf, uint32_t nan_bin,
+                                                         uint8_t *__restrict__ Xb, int stride)
+{
+    __shared__ float u[128 * kBinStrideLds];
+    for (int e = threadIdx.x; e < nf * kBinSlots; e += kBinThreads)
+        u[(e >> 8) * kBinStrideLds + (e & 255)] = U[e];
+    __syncthreads();
+    const int f = threadIdx.x & 127;
+    const int sub = threadIdx.x >> 7;                 // 8 rows per pass
+    if (f >= stride) return;
+    const float *uf = u + f * kBinStrideLds;
+    for (int64_t r = (int64_t)blockIdx.x * 8 + sub; r < R; r += (int64_t)gridDim.x * 8) {
+        uint32_t bin = 0;
+        if (f < nf) {
+            const float x = X[r * ld + f];
+            if (x != x) {
+                bin = nan_bin;
+            } else {
+#pragma unroll
+                for (int step = 128; step > 0; step >>= 1) bin += (uf[bin + step - 1] <= x) ? step : 0;
+            }
+        }
+        Xb[r * stride + f] = (uint8_t)bin;
+    }
+}
+
+template <int TC, int D>
+__global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__restrict__ chunks, int n_chunks,
+                                                              const uint8_t *__restrict__ Xb, int64_t R,
+                                                              int stride, int groups_per_xcd,
+                                                              int64_t rows_per_group, float *__restrict__ partial)
+{
+    constexpr int NS = 1 << D;
+    constexpr int NODE_B = NS * TC * 2;
+    constexpr int CHUNK_B = NS * TC * 6;
+    constexpr int RPI = 64 / TC;                       // rows per lane group
+    constexpr int ROWS_PER_WAVE = kTileRows / kWaves;  // 16
+    constexpr int ITER = ROWS_PER_WAVE / (RPI * kIlp);
+    static_assert(ITER >= 1 && ITER * RPI * kIlp == ROWS_PER_WAVE, "tile shape");
+    __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kTileStride + kTileRows * 4];
+    const uint16_t *nodes = reinterpret_cast<const uint16_t *>(lds);
+    const float *leaves = reinterpret_cast<const float *>(lds + NODE_B);
+    uint8_t *bins = lds + CHUNK_B;
+    float *rowsum = reinterpret_cast<float *>(lds + CHUNK_B + kTileRows * kTileStride);
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int t = lane % TC, s = lane / TC;
+    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+    const int slots = gridDim.x / kXcds;
+    const int items = n_chunks * groups_per_xcd;
+    const int words = stride >> 2;                     // dwords per bin row
+
+    for (int item = slot; item < items; item += slots) {
+        const int c = item % n_chunks, sub = item / n_chunks;
+        const int64_t g = (int64_t)xcd * groups_per_xcd + sub;
+        const int64_t r_begin = g * rows_per_group;
+        const int64_t r_end = r_begin + rows_per_group < R ? r_begin + rows_per_group : R;
+        __syncthreads();
+        {   // chunk image -> LDS
+            const uint4 *src = reinterpret_cast<const uint4 *>(chunks + (size_t)c * CHUNK_B);
+            uint4 *dst = reinterpret_cast<uint4 *>(lds);
+            for (int e = threadIdx.x; e < CHUNK_B / 16; e += 64 * kWaves) dst[e] = src[e];
+        }
+        for (int64_t t0 = r_begin; t0 < r_end; t0 += kTileRows) {
+            const int n_tile = (int)(r_end - t0 < kTileRows ? r_end - t0 : kTileRows);
+            __syncthreads();
+            for (int e = threadIdx.x; e < n_tile * words; e += 64 * kWaves) {
+                const int rr = e / words, w = e - rr * words;
+                const uint32_t v = reinterpret_cast<const uint32_t *>(Xb + (t0 + rr) * stride)[w];
+                *reinterpret_cast<uint32_t *>(bins + rr * kTileStride + 4 * w) = v;
+            }
+            __syncthreads();
+#pragma unroll 1
+            for (int it = 0; it < ITER; ++it) {
+                int node[kIlp];
+                const uint8_t *rowp[kIlp];
+#pragma unroll
+                for (int a = 0; a < kIlp; ++a) {
+                    const int row = wave * ROWS_PER_WAVE + (it * kIlp + a) * RPI + s;
+                    rowp[a] = bins + row * kTileStride;
+                    node[a] = 1;
+                }
+#pragma unroll
+                for (int l = 0; l < D; ++l) {
+                    uint32_t code[kIlp];
+#pragma unroll
+                    for (int a = 0; a < kIlp; ++a) code[a] = nodes[node[a] * TC + t];
+#pragma unroll
+                    for (int a = 0; a < kIlp; ++a) {
+                        const uint32_t xb = rowp[a][code[a] & 0xffu];
+                        node[a] = 2 * node[a] + (xb > (code[a] >> 8) ? 1 : 0);
+                    }
+                }
+#pragma unroll
+                for (int a = 0; a < kIlp; ++a) {
+                    float v = leaves[(node[a] - NS) * TC + t];
+#pragma unroll
+                    for (int m = TC / 2; m > 0; m >>= 1) v += __shfl_xor(v, m, 64);
+                    if (t == 0) rowsum[wave * ROWS_PER_WAVE + (it * kIlp + a) * RPI + s] = v;
+                }
+            }
+            __syncthreads();
+            for (int e = threadIdx.x; e < n_tile; e += 64 * kWaves) partial[(int64_t)c * R + t0 + e] = rowsum[e];
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_reduce(const float *__restrict__ partial, int n_chunks, int64_t R,
+                                                 float base, float *__restrict__ scores)
+{
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= R) return;
+    float acc = base;
+    for (int c = 0; c < n_chunks; ++c) acc += partial[(int64_t)c * R + r];
+    scores[r] = acc;
+}
+
+template <int TC, int D>
+hipError_t launch_traverse_tc(const uint8_t *chunks, int n_chunks, const uint8_t *Xb, int64_t R, int stride,
+                              float *partial, hipStream_t s)
+{
+    const int groups = n_chunks >= kSlotsPerXcd ? 1 : (kSlotsPerXcd + n_chunks - 1) / n_chunks;
+    const int64_t n_groups = (int64_t)kXcds * groups;
+    int64_t per = (R + n_groups - 1) / n_groups;
+    per = (per + kTileRows - 1) / kTileRows * kTileRows;
+    hipLaunchKernelGGL((k_traverse<TC, D>), dim3(kXcds * kSlotsPerXcd), dim3(64 * kWaves), 0, s, chunks,
+                       n_chunks, Xb, R, stride, groups, per, partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_traverse(int depth, const uint8_t *chunks, int n_chunks, const uint8_t *Xb, int64_t R,
+                           int stride, float *partial, hipStream_t s)
+{
+    switch (depth) {
+    case 1: return launch_traverse_tc<64, 1>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 2: return launch_traverse_tc<64, 2>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 3: return launch_traverse_tc<64, 3>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 4: return launch_traverse_tc<64, 4>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 5: return launch_traverse_tc<64, 5>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 6: return launch_traverse_tc<64, 6>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 7: return launch_traverse_tc<64, 7>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 8: return launch_traverse_tc<64, 8>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 9: return launch_traverse_tc<32, 9>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 10: return launch_traverse_tc<16, 10>(chunks, n_chunks, Xb, R, stride, partial, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
 hipError_t launch_forest_score(const hwsel_forest_t &f, const float *X, int64_t R, int64_t ld,
                                float *scores, hipStream_t s)
 {
@@ -82,6 +312,98 @@ hipError_t launch_forest_leaves(const hwsel_forest_t &f, const float *X, int64_t
 {
     const dim3 grid((unsigned)((n_rows + 255) / 256)), block(256);
     hipLaunchKernelGGL(k_forest_leaves, grid, block, 0, s, to_dev(f), X, R, ld, rows, n_rows, leaf_idx);
+    return hipGetLastError();
+}
+
+bool packable(const hwsel_forest_t &f) { return f.depth >= 1 && f.depth <= 10 && f.n_features <= 128; }
+
+size_t packed_bytes(const hwsel_forest_t &f) { return geometry(f).total; }
+
+size_t packed_workspace_bytes(const hwsel_forest_t &f, int64_t R)
+{
+    const PackGeom g = geometry(f);
+    return align256((size_t)R * g.stride) + (size_t)g.n_chunks * (size_t)R * sizeof(float);
+}
+
+// Copy the forest to the host, build the binned chunk images, upload them.
+PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
+{
+    const PackGeom g = geometry(f);
+    const int64_t n_int = ((int64_t)1 << f.depth) - 1;
+    const int64_t nn = n_int * f.n_trees, nl = (n_int + 1) * f.n_trees;
+    std::vector<uint8_t> feat(nn);
+    std::vector<float> thr(nn), leaf(nl);
+    if (hipMemcpyAsync(feat.data(), f.node_feature, nn, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(thr.data(), f.node_threshold, nn * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(leaf.data(), f.leaf_value, nl * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return PackStatus::hip_error;
+    // distinct thresholds per feature
+    std::vector<std::vector<float>> U(f.n_features);
+    for (int64_t e = 0; e < nn; ++e) {
+        if (feat[e] >= f.n_features) return PackStatus::bad_feature;
+        if (thr[e] != thr[e]) return PackStatus::nan_threshold;
+        U[feat[e]].push_back(thr[e] == 0.0f ? 0.0f : thr[e]);
+    }
+    std::vector<uint8_t> img(g.total, 0);
+    float *table = reinterpret_cast<float *>(img.data() + 256);
+    for (int j = 0; j < f.n_features; ++j) {
+        auto &u = U[j];
+        std::sort(u.begin(), u.end());
+        u.erase(std::unique(u.begin(), u.end()), u.end());
+        if (u.size() > 255) return PackStatus::too_many_thresholds;
+        for (int k = 0; k < kBinSlots; ++k)
+            table[j * kBinSlots + k] = k < (int)u.size() ? u[k] : __builtin_inff();
+    }
+    uint8_t *chunk0 = img.data() + 256 + g.thr_bytes;
+    for (int c = 0; c < g.n_chunks; ++c) {
+        uint16_t *nodes = reinterpret_cast<uint16_t *>(chunk0 + (size_t)c * g.chunk_bytes);
+        float *leaves = reinterpret_cast<float *>(chunk0 + (size_t)c * g.chunk_bytes + g.node_bytes);
+        for (int tt = 0; tt < g.tc; ++tt) {
+            const int64_t tree = (int64_t)c * g.tc + tt;
+            if (tree >= f.n_trees) continue;   // padding trees: zero codes, zero leaves
+            for (int64_t n = 0; n < n_int; ++n) {
+                const uint8_t fj = feat[tree * n_int + n];
+                float v = thr[tree * n_int + n];
+                v = v == 0.0f ? 0.0f : v;
+                const auto &u = U[fj];
+                const int rank = (int)(std::lower_bound(u.begin(), u.end(), v) - u.begin());
+                nodes[(n + 1) * g.tc + tt] = (uint16_t)(fj | (rank << 8));
+            }
+            for (int64_t l = 0; l <= n_int; ++l) leaves[l * g.tc + tt] = leaf[tree * (n_int + 1) + l];
+        }
+    }
+    int32_t *hdr = reinterpret_cast<int32_t *>(img.data());
+    hdr[0] = 0x48575346;   // "FSWH"
+    hdr[1] = 1;
+    hdr[2] = f.n_trees; hdr[3] = f.depth; hdr[4] = f.n_features; hdr[5] = g.tc; hdr[6] = g.n_chunks;
+    if (hipMemcpyAsync(packed, img.data(), g.total, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return PackStatus::hip_error;
+    return PackStatus::ok;
+}
+
+hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
+                                int64_t ld, float *scores, void *workspace, hipStream_t s)
+{
+    const PackGeom g = geometry(f);
+    const uint8_t *base = static_cast<const uint8_t *>(packed);
+    const float *U = reinterpret_cast<const float *>(base + 256);
+    const uint8_t *chunks = base + 256 + g.thr_bytes;
+    uint8_t *Xb = static_cast<uint8_t *>(workspace);
+    float *partial = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + align256((size_t)R * g.stride));
+    const uint32_t nan_bin = (f.flags & 1u) ? 0u : 255u;
+    int dev = 0, n_cu = 256;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+        n_cu = 256;
+    hipLaunchKernelGGL(k_bin, dim3(n_cu), dim3(kBinThreads), 0, s, X, R, ld, U, f.n_features, nan_bin, Xb, g.stride);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_traverse(f.depth, chunks, g.n_chunks, Xb, R, g.stride, partial, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_reduce, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
+                       f.base_score, scores);
     return hipGetLastError();
 }
 

@@ -35,6 +35,15 @@ hipError_t launch_forest_leaves(const hwsel_forest_t &f, const float *X, int64_t
                                 const int64_t *rows, int64_t n_rows, uint16_t *leaf_idx,
                                 hipStream_t s);
 
+// Packed forests (see forest.hip).
+enum class PackStatus { ok, hip_error, bad_feature, nan_threshold, too_many_thresholds };
+bool packable(const hwsel_forest_t &f);
+size_t packed_bytes(const hwsel_forest_t &f);
+size_t packed_workspace_bytes(const hwsel_forest_t &f, int64_t R);
+PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s);
+hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
+                                int64_t ld, float *scores, void *workspace, hipStream_t s);
+
 hipError_t launch_mlp(const hwsel_mlp_t &m, const float *X, int64_t R, int64_t ld, float *scores,
                       hipStream_t s);
 

@@ -70,7 +70,10 @@ def lib() -> C.CDLL:
         L.hwsel_last_error.restype = C.c_char_p
         vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
         L.hwsel_features.argtypes = [hwsel_hw_t, vp, i32, vp, C.POINTER(hwsel_cands_t), i64, i32, vp, i64, vp]
-        L.hwsel_forest_score.argtypes = [C.POINTER(hwsel_forest_t), vp, i64, i64, vp, vp]
+        L.hwsel_forest_score.argtypes = [C.POINTER(hwsel_forest_t), vp, vp, i64, i64, vp, vp, C.c_size_t, vp]
+        L.hwsel_forest_pack_bytes.argtypes = [C.POINTER(hwsel_forest_t), C.POINTER(C.c_size_t)]
+        L.hwsel_forest_pack.argtypes = [C.POINTER(hwsel_forest_t), vp, C.c_size_t, vp]
+        L.hwsel_forest_workspace_bytes.argtypes = [C.POINTER(hwsel_forest_t), i64, C.POINTER(C.c_size_t)]
         L.hwsel_forest_leaves.argtypes = [C.POINTER(hwsel_forest_t), vp, i64, i64, vp, i64, vp, vp]
         L.hwsel_mlp_score.argtypes = [C.POINTER(hwsel_mlp_t), vp, i64, i64, vp, vp]
         L.hwsel_topk_per_problem.argtypes = [vp, vp, i32, i32, vp, vp, vp]
@@ -151,14 +154,49 @@ def forest_struct(f: dict) -> hwsel_forest_t:
                           _ptr(f["leaf_value"]))
 
 
+def hwsel_forest_pack_bytes(forest: dict) -> int:
+    n = C.c_size_t(0)
+    s = forest_struct(forest)
+    _check("hwsel_forest_pack_bytes", lib().hwsel_forest_pack_bytes(C.byref(s), C.byref(n)))
+    return int(n.value)
+
+
+def hwsel_forest_pack(forest: dict, packed: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Pack a device-resident forest once; returns the packed image (uint8)."""
+    nbytes = hwsel_forest_pack_bytes(forest)
+    if packed is None:
+        packed = torch.empty(nbytes, dtype=torch.uint8, device=forest["node_feature"].device)
+    s = forest_struct(forest)
+    _check("hwsel_forest_pack", lib().hwsel_forest_pack(C.byref(s), _ptr(packed), packed.numel(),
+                                                        _stream(stream)))
+    return packed
+
+
+def hwsel_forest_workspace_bytes(forest: dict, R: int) -> int:
+    n = C.c_size_t(0)
+    s = forest_struct(forest)
+    _check("hwsel_forest_workspace_bytes", lib().hwsel_forest_workspace_bytes(C.byref(s), R, C.byref(n)))
+    return int(n.value)
+
+
 def hwsel_forest_score(forest: dict, X: torch.Tensor, scores: torch.Tensor | None = None,
+                       packed: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
                        stream=None) -> torch.Tensor:
+    """Score rows of X.  With ``packed`` (from hwsel_forest_pack) the fast
+    path runs and ``workspace`` (allocated here if None) holds its bins and
+    partial sums."""
     R = X.shape[0]
     if scores is None:
         scores = torch.empty(R, dtype=torch.float32, device=X.device)
+    ws_bytes = 0
+    if packed is not None:
+        if workspace is None:
+            workspace = torch.empty(hwsel_forest_workspace_bytes(forest, R), dtype=torch.uint8, device=X.device)
+        ws_bytes = workspace.numel() * workspace.element_size()
     s = forest_struct(forest)
     _check("hwsel_forest_score", lib().hwsel_forest_score(
-        C.byref(s), _ptr(X), R, X.stride(0), _ptr(scores), _stream(stream)))
+        C.byref(s), _ptr(packed), _ptr(X), R, X.stride(0), _ptr(scores), _ptr(workspace), ws_bytes,
+        _stream(stream)))
     return scores
 
 

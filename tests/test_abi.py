@@ -73,7 +73,7 @@ def test_forest_rejects(L, over, status):
     R = over.pop("R", 100)
     f.update(over)
     s = hwsel.forest_struct(f)
-    assert L.hwsel_forest_score(C.byref(s), FAKE, R, ld, FAKE, None) == status
+    assert L.hwsel_forest_score(C.byref(s), None, FAKE, R, ld, FAKE, None, 0, None) == status
     assert L.hwsel_forest_leaves(C.byref(s), FAKE, R, ld, FAKE, 5, FAKE, None) == status
 
 
@@ -99,3 +99,24 @@ def test_select_rejects(L, P, k, status):
     assert L.hwsel_topk_per_problem(FAKE, FAKE, P, k, FAKE, None, None) == status
     assert L.hwsel_regret(FAKE, FAKE, P, FAKE, k, FAKE, None, None, None) == status
     assert L.hwsel_regret(None, FAKE, 4, FAKE, 5, FAKE, None, None, None) == 1
+
+
+def test_forest_packed_rejects(L):
+    f = dict(n_trees=10, depth=10, n_features=128, flags=1, base_score=0.0, node_feature=FAKE,
+             node_threshold=FAKE, leaf_value=FAKE)
+    s = hwsel.forest_struct(f)
+    n = C.c_size_t(0)
+    assert L.hwsel_forest_pack_bytes(C.byref(s), C.byref(n)) == 0 and n.value > 0
+    ws = C.c_size_t(0)
+    assert L.hwsel_forest_workspace_bytes(C.byref(s), 1000, C.byref(ws)) == 0
+    assert ws.value >= 1000 * 128 + 1000 * 4        # bins + one chunk of (up to 16) trees
+    # short workspace, misaligned workspace, misaligned image
+    assert L.hwsel_forest_score(C.byref(s), FAKE, FAKE, 1000, 128, FAKE, FAKE, ws.value - 1, None) == 1
+    assert L.hwsel_forest_score(C.byref(s), FAKE, FAKE, 1000, 128, FAKE, FAKE + 16, ws.value, None) == 1
+    assert L.hwsel_forest_score(C.byref(s), FAKE + 4, FAKE, 1000, 128, FAKE, FAKE, ws.value, None) == 1
+    assert L.hwsel_forest_pack(C.byref(s), FAKE, n.value - 1, None) == 1
+    deep = hwsel.forest_struct(dict(f, depth=11))
+    assert L.hwsel_forest_pack_bytes(C.byref(deep), C.byref(n)) == 2
+    wide = hwsel.forest_struct(dict(f, n_features=200))
+    assert L.hwsel_forest_pack_bytes(C.byref(wide), C.byref(n)) == 2
+    assert L.hwsel_forest_score(C.byref(wide), FAKE, FAKE, 1000, 200, FAKE, FAKE, 1 << 30, None) == 2

@@ -47,12 +47,28 @@ def test_forest_tiny_all_rows(tiny):
     say("forest tiny")
     ref_X = oracle.features(w.hw, w.problems, w.seg, w.cands, 64)
     Xd = torch.from_numpy(ref_X).cuda()             # identical input on both sides
-    s = hwsel.hwsel_forest_score(d.forest, Xd).cpu().numpy()
     rows = torch.arange(len(ref_X), dtype=torch.int64, device="cuda")
     li = hwsel.hwsel_forest_leaves(d.forest, Xd, rows).cpu().numpy().view(np.uint16)
     o, oli = oracle.forest(w.forest, ref_X, leaves=True)
     assert np.array_equal(li, oli)
-    say(f"  score err/bound max {assert_forest_scores(s, o, path_l1(w.forest, oli)):.3g}")
+    l1 = path_l1(w.forest, oli)
+    s = hwsel.hwsel_forest_score(d.forest, Xd).cpu().numpy()
+    say(f"  direct walk: score err/bound max {assert_forest_scores(s, o, l1):.3g}")
+    packed = hwsel.hwsel_forest_pack(d.forest)
+    sp = hwsel.hwsel_forest_score(d.forest, Xd, packed=packed).cpu().numpy()
+    say(f"  packed: score err/bound max {assert_forest_scores(sp, o, l1):.3g}")
+    sp2 = hwsel.hwsel_forest_score(d.forest, Xd, packed=packed).cpu().numpy()
+    assert np.array_equal(sp.view(np.uint32), sp2.view(np.uint32))      # run-to-run identical
+
+
+def _leaf_probe(forest: dict, t0: int) -> dict:
+    """Same nodes, leaves zero except tree t0 whose leaf l holds the value l:
+    the ensemble's score is exactly the leaf index reached in tree t0."""
+    f = dict(forest)
+    lv = np.zeros_like(forest["leaf_value"])
+    lv[t0] = np.arange(lv.shape[1], dtype=np.float32)
+    f["leaf_value"] = lv
+    return f
 
 
 def test_selection_tiny_end_to_end(tiny):
@@ -134,14 +150,28 @@ def test_forest_workload_full_size(name):
     Xs = X.index_select(0, rows_d).cpu().numpy()
     ref = oracle.features(w.hw, w.problems, w.seg, w.cands, cfg.n_features, rows)
     say(f"  features {compare_features(Xs, ref, cfg.n_features)}")
-    say(f"workload {name}: forest {cfg.trees}x{cfg.depth}")
-    s = hwsel.hwsel_forest_score(d.forest, X)
+    say(f"workload {name}: forest {cfg.trees}x{cfg.depth}, packed path as benchmarked")
+    packed = hwsel.hwsel_forest_pack(d.forest)
+    ws = torch.empty(hwsel.hwsel_forest_workspace_bytes(d.forest, cfg.rows), dtype=torch.uint8, device="cuda")
+    s = hwsel.hwsel_forest_score(d.forest, X, packed=packed, workspace=ws)
     li = hwsel.hwsel_forest_leaves(d.forest, X, rows_d).cpu().numpy().view(np.uint16)
     o, oli = oracle.forest(w.forest, ref, leaves=True)
     assert np.array_equal(li, oli)
+    l1 = path_l1(w.forest, oli)
     g = s.index_select(0, rows_d).cpu().numpy()
-    say(f"  forest err/bound {assert_forest_scores(g, o, path_l1(w.forest, oli)):.3g}")
+    say(f"  packed forest err/bound {assert_forest_scores(g, o, l1):.3g}")
     assert bool(torch.isfinite(s).all())
+    # leaf indices of the packed traversal itself, for a few trees, on every row
+    for t0 in (0, cfg.trees // 2 + 1, cfg.trees - 1):
+        probe = _leaf_probe(w.forest, t0)
+        from _gpu_util import forest_to_device
+        pd = forest_to_device(probe)
+        sp = hwsel.hwsel_forest_score(pd, X, packed=hwsel.hwsel_forest_pack(pd), workspace=ws)
+        assert np.array_equal(sp.index_select(0, rows_d).cpu().numpy(), oli[:, t0].astype(np.float32)), t0
+        # and on every row, against the direct walk's leaves
+        sg = hwsel.hwsel_forest_score(pd, X)
+        assert bool((sp == sg).all()), t0
+    say("  packed leaf indices match for probed trees")
     say(f"workload {name}: top-k / regret")
     idx, vals = hwsel.hwsel_topk_per_problem(s, d.seg, cfg.k)
     r1, rk, best = hwsel.hwsel_regret(d.runtimes, d.seg, idx)
