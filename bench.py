@@ -97,7 +97,8 @@ def main():
     for n in ("node_feature", "node_threshold", "leaf_value"):
         forest[n] = hwsel.to_device(w.forest[n], dev)
     mlp = {n: hwsel.to_device(v, dev) for n, v in mw.items()}
-    log("pack forest (once per model)")
+    log("pack forest and MLP (once per model)")
+    mlp_packed = hwsel.hwsel_mlp_pack(mlp)
     packed = hwsel.hwsel_forest_pack(forest)
     ws = torch.empty(hwsel.hwsel_forest_workspace_bytes(forest, R), dtype=torch.uint8, device=dev)
     X = torch.empty((R, F), dtype=torch.float32, device=dev)
@@ -123,7 +124,7 @@ def main():
         mark(3)
         hwsel.hwsel_regret(rt, seg, outs[0][0], *regs[0])
         mark(4)
-        hwsel.hwsel_mlp_score(mlp, X, scores=s_m)
+        hwsel.hwsel_mlp_score(mlp, X, scores=s_m, packed=mlp_packed)
         mark(5)
         hwsel.hwsel_topk_per_problem(s_m, seg, k, idx=outs[1][0], vals=outs[1][1])
         mark(6)

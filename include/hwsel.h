@@ -199,12 +199,25 @@ typedef struct hwsel_mlp {
 } hwsel_mlp_t;
 
 /*
- * scores[r] = MLP(X[r][0..128)) for r < R.  X: fp32 [R][ld], ld >= 128,
- * ld % 4 == 0, 16-byte aligned.  Returns HWSEL_EINVAL for null pointers,
- * R < 1, bad ld/alignment; HWSEL_EUNSUPPORTED for other widths.
+ * Packing: a one-time rearrangement of W1..W3 into the fragment order of the
+ * bf16 matrix-core instructions (asynchronous on `stream`; the weights must
+ * not change until it has run).  `packed` is device memory of
+ * hwsel_mlp_pack_bytes() bytes, 16-byte aligned.  Returns HWSEL_EINVAL for
+ * null pointers or a short buffer, HWSEL_EUNSUPPORTED for other widths.
  */
-int hwsel_mlp_score(const hwsel_mlp_t *m, const float *X, int64_t R, int64_t ld, float *scores,
-                    void *stream);
+int hwsel_mlp_pack_bytes(const hwsel_mlp_t *m, size_t *bytes);
+int hwsel_mlp_pack(const hwsel_mlp_t *m, void *packed, size_t bytes, void *stream);
+
+/*
+ * scores[r] = MLP(X[r][0..128)) for r < R.  X: fp32 [R][ld], ld >= 128,
+ * ld % 4 == 0, 16-byte aligned.  packed: NULL for the fp32-FMA row-block
+ * kernel, or the image hwsel_mlp_pack wrote for these weights (matrix-core
+ * kernel; mean, inv_std and b1..b3 must then be 16-byte aligned and W4
+ * 8-byte aligned).  Returns HWSEL_EINVAL for null pointers, R < 1, bad
+ * ld/alignment; HWSEL_EUNSUPPORTED for other widths.
+ */
+int hwsel_mlp_score(const hwsel_mlp_t *m, const void *packed, const float *X, int64_t R, int64_t ld,
+                    float *scores, void *stream);
 
 /*
  * Per-problem selection, eq. (selection) generalised to the k best:

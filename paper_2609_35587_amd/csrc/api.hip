@@ -162,19 +162,51 @@ int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int6
     return launched(hwsel::launch_forest_leaves(*f, X, R, ld, rows, n_rows, leaf_idx, (hipStream_t)stream), fn);
 }
 
-int hwsel_mlp_score(const hwsel_mlp_t *m, const float *X, int64_t R, int64_t ld, float *scores, void *stream)
+static int check_mlp(const hwsel_mlp_t *m, const char *fn)
 {
-    static const char *fn = "hwsel_mlp_score";
-    if (!m || !X || !scores || !m->mean || !m->inv_std || !m->W1 || !m->W2 || !m->W3 || !m->W4 || !m->b1 ||
-        !m->b2 || !m->b3 || !m->b4)
+    if (!m || !m->mean || !m->inv_std || !m->W1 || !m->W2 || !m->W3 || !m->W4 || !m->b1 || !m->b2 || !m->b3 ||
+        !m->b4)
         return fail(HWSEL_EINVAL, fn, "null pointer");
     if (m->n_in != 128 || m->h1 != 512 || m->h2 != 512 || m->h3 != 256)
         return fail(HWSEL_EUNSUPPORTED, fn, "widths %d-%d-%d-%d (supported: 128-512-512-256)", m->n_in, m->h1,
                     m->h2, m->h3);
+    return HWSEL_OK;
+}
+
+int hwsel_mlp_pack_bytes(const hwsel_mlp_t *m, size_t *bytes)
+{
+    static const char *fn = "hwsel_mlp_pack_bytes";
+    if (!bytes) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (int s = check_mlp(m, fn)) return s;
+    *bytes = hwsel::mlp_packed_bytes();
+    g_err[0] = 0;
+    return HWSEL_OK;
+}
+
+int hwsel_mlp_pack(const hwsel_mlp_t *m, void *packed, size_t bytes, void *stream)
+{
+    static const char *fn = "hwsel_mlp_pack";
+    if (int s = check_mlp(m, fn)) return s;
+    if (!packed) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (bytes < hwsel::mlp_packed_bytes()) return fail(HWSEL_EINVAL, fn, "bytes=%zu < %zu", bytes, hwsel::mlp_packed_bytes());
+    if (!aligned16(packed)) return fail(HWSEL_EINVAL, fn, "packed not 16-byte aligned");
+    return launched(hwsel::launch_mlp_pack(*m, packed, (hipStream_t)stream), fn);
+}
+
+int hwsel_mlp_score(const hwsel_mlp_t *m, const void *packed, const float *X, int64_t R, int64_t ld, float *scores,
+                    void *stream)
+{
+    static const char *fn = "hwsel_mlp_score";
+    if (int s = check_mlp(m, fn)) return s;
+    if (!X || !scores) return fail(HWSEL_EINVAL, fn, "null pointer");
     if (R < 1) return fail(HWSEL_EINVAL, fn, "R=%lld", (long long)R);
     if (ld < 128 || ld % 4 != 0) return fail(HWSEL_EINVAL, fn, "ld=%lld", (long long)ld);
     if (!aligned16(X)) return fail(HWSEL_EINVAL, fn, "X not 16-byte aligned");
-    return launched(hwsel::launch_mlp(*m, X, R, ld, scores, (hipStream_t)stream), fn);
+    if (!packed) return launched(hwsel::launch_mlp(*m, X, R, ld, scores, (hipStream_t)stream), fn);
+    if (!aligned16(packed) || !aligned16(m->mean) || !aligned16(m->inv_std) || !aligned16(m->b1) ||
+        !aligned16(m->b2) || !aligned16(m->b3) || ((uintptr_t)m->W4 & 7u) != 0)
+        return fail(HWSEL_EINVAL, fn, "misaligned packed weights, statistics or biases");
+    return launched(hwsel::launch_mlp_packed(*m, packed, X, R, ld, scores, (hipStream_t)stream), fn);
 }
 
 int hwsel_topk_per_problem(const float *scores, const int64_t *seg_offsets, int32_t P, int32_t k, int32_t *idx,

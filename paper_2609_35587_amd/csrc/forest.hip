@@ -107,7 +107,6 @@ constexpr int kBinStrideLds = 257;    // LDS row stride (floats) of the bin tabl
 constexpr int kTileRows = 256;        // rows of bins per LDS tile
 constexpr int kTileStride = 132;      // LDS bytes per bin row (33 dwords)
 constexpr int kWaves = 16;            // waves per traversal workgroup
-constexpr int kIlp = 4;               // row groups in flight per wave
 constexpr int kXcds = 8;
 constexpr int kSlotsPerXcd = 32;      // one workgroup per CU
 constexpr int kBinThreads = 1024;
@@ -153,22 +152,77 @@ __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict_
         u[(e >> 8) * kBinStrideLds + (e & 255)] = U[e];
     __syncthreads();
     const int f = threadIdx.x & 127;
-    const int sub = threadIdx.x >> 7;                 // 8 rows per pass
+    const int sub = threadIdx.x >> 7;                 // 8 row lanes per block
     if (f >= stride) return;
     const float *uf = u + f * kBinStrideLds;
-    for (int64_t r = (int64_t)blockIdx.x * 8 + sub; r < R; r += (int64_t)gridDim.x * 8) {
-        uint32_t bin = 0;
-        if (f < nf) {
-            const float x = X[r * ld + f];
-            if (x != x) {
-                bin = nan_bin;
-            } else {
+    constexpr int kRowsPerThread = 4;                 // independent searches in flight
+    const int64_t step_rows = (int64_t)gridDim.x * 8 * kRowsPerThread;
+    for (int64_t r0 = ((int64_t)blockIdx.x * 8 + sub) * kRowsPerThread; r0 < R; r0 += step_rows) {
+        float x[kRowsPerThread];
+        uint32_t bin[kRowsPerThread];
 #pragma unroll
-                for (int step = 128; step > 0; step >>= 1) bin += (uf[bin + step - 1] <= x) ? step : 0;
-            }
+        for (int q = 0; q < kRowsPerThread; ++q) {
+            x[q] = (f < nf && r0 + q < R) ? X[(r0 + q) * ld + f] : 0.0f;
+            bin[q] = 0;
         }
-        Xb[r * stride + f] = (uint8_t)bin;
+#pragma unroll
+        for (int step = 128; step > 0; step >>= 1) {
+#pragma unroll
+            for (int q = 0; q < kRowsPerThread; ++q) bin[q] += (uf[bin[q] + step - 1] <= x[q]) ? step : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < kRowsPerThread; ++q) {
+            if (r0 + q >= R) break;
+            uint32_t b = bin[q];
+            if (x[q] != x[q]) b = nan_bin;
+            if (f >= nf) b = 0;
+            Xb[(r0 + q) * stride + f] = (uint8_t)b;
+        }
     }
+}
+
+// One level of a walk: node <- 2*node + (bin > rank), with rank the high
+// byte of the node code.  Subtract-with-borrow leaves (bin > rank) in VCC and
+// add-with-carry folds it in: two VALU instructions per visit.
+__device__ __forceinline__ int descend(int node, uint32_t code, uint32_t bin)
+{
+    int out;
+    asm("v_sub_co_u32_sdwa %0, vcc, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD\n\t"
+        "v_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
+        : "=&v"(out)
+        : "v"(code), "v"(bin), "v"(node)
+        : "vcc");
+    return out;
+}
+
+template <int CTRL, int ROW_MASK, bool ZERO_FILL>
+__device__ __forceinline__ float dpp_add(float v)
+{
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xf, ZERO_FILL));
+}
+
+// Sum over each aligned group of TC lanes (TC in {16, 32, 64}) with DPP:
+// an inclusive scan inside 16-lane rows, then row broadcasts.  The last lane
+// of each group ends with the group's total, always in the same order.
+template <int TC>
+__device__ __forceinline__ float group_total(float v)
+{
+    static_assert(TC == 16 || TC == 32 || TC == 64, "group width");
+    v = dpp_add<0x111, 0xf, true>(v);   // row_shr:1
+    v = dpp_add<0x112, 0xf, true>(v);   // row_shr:2
+    v = dpp_add<0x114, 0xf, true>(v);   // row_shr:4
+    v = dpp_add<0x118, 0xf, true>(v);   // row_shr:8
+    if constexpr (TC >= 32) v = dpp_add<0x142, 0xa, false>(v);   // row_bcast:15 into rows 1, 3
+    if constexpr (TC >= 64) v = dpp_add<0x143, 0xc, false>(v);   // row_bcast:31 into rows 2, 3
+    return v;
+}
+
+// Position of tree t's node codes inside a heap slot.  With 64 trees a slot
+// is 128 bytes; storing tree t at 2*(t % 32) + t / 32 gives the 32 lanes of
+// each half-wave 32 distinct banks.
+__host__ __device__ __forceinline__ int node_pos(int t, int tc)
+{
+    return tc == 64 ? 2 * (t & 31) + (t >> 5) : t;
 }
 
 template <int TC, int D>
@@ -182,8 +236,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
     constexpr int CHUNK_B = NS * TC * 6;
     constexpr int RPI = 64 / TC;                       // rows per lane group
     constexpr int ROWS_PER_WAVE = kTileRows / kWaves;  // 16
-    constexpr int ITER = ROWS_PER_WAVE / (RPI * kIlp);
-    static_assert(ITER >= 1 && ITER * RPI * kIlp == ROWS_PER_WAVE, "tile shape");
+    constexpr int ILP = ROWS_PER_WAVE / RPI < 8 ? ROWS_PER_WAVE / RPI : 8;   // row groups in flight
+    constexpr int ITER = ROWS_PER_WAVE / (RPI * ILP);
+    static_assert(ITER >= 1 && ITER * RPI * ILP == ROWS_PER_WAVE, "tile shape");
     __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kTileStride + kTileRows * 4];
     const uint16_t *nodes = reinterpret_cast<const uint16_t *>(lds);
     const float *leaves = reinterpret_cast<const float *>(lds + NODE_B);
@@ -192,10 +247,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int t = lane % TC, s = lane / TC;
+    const int npos = node_pos(t, TC);
     const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
     const int slots = gridDim.x / kXcds;
     const int items = n_chunks * groups_per_xcd;
-    const int words = stride >> 2;                     // dwords per bin row
 
     for (int item = slot; item < items; item += slots) {
         const int c = item % n_chunks, sub = item / n_chunks;
@@ -208,42 +263,59 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
             uint4 *dst = reinterpret_cast<uint4 *>(lds);
             for (int e = threadIdx.x; e < CHUNK_B / 16; e += 64 * kWaves) dst[e] = src[e];
         }
+        // Bin tiles stream through registers: tile k+1 is fetched from global
+        // memory while tile k is walked from LDS.
+        constexpr int kVec = kTileRows * 128 / 16 / (64 * kWaves);   // uint4 per thread (2)
+        const int vpr = stride >> 4;                                  // uint4 per bin row
+        uint4 pre[kVec];
+        auto fetch = [&](int64_t t0) {
+            const int n = (int)(r_end - t0 < kTileRows ? r_end - t0 : kTileRows);
+#pragma unroll
+            for (int q = 0; q < kVec; ++q) {
+                const int e = threadIdx.x + q * 64 * kWaves;
+                const int rr = e / vpr, w = e - rr * vpr;
+                pre[q] = (rr < n && t0 < r_end)
+                             ? reinterpret_cast<const uint4 *>(Xb + (t0 + rr) * stride)[w]
+                             : make_uint4(0, 0, 0, 0);
+            }
+        };
+        fetch(r_begin);
         for (int64_t t0 = r_begin; t0 < r_end; t0 += kTileRows) {
             const int n_tile = (int)(r_end - t0 < kTileRows ? r_end - t0 : kTileRows);
             __syncthreads();
-            for (int e = threadIdx.x; e < n_tile * words; e += 64 * kWaves) {
-                const int rr = e / words, w = e - rr * words;
-                const uint32_t v = reinterpret_cast<const uint32_t *>(Xb + (t0 + rr) * stride)[w];
-                *reinterpret_cast<uint32_t *>(bins + rr * kTileStride + 4 * w) = v;
+#pragma unroll
+            for (int q = 0; q < kVec; ++q) {
+                const int e = threadIdx.x + q * 64 * kWaves;
+                const int rr = e / vpr, w = e - rr * vpr;
+                if (rr < kTileRows) {
+                    uint32_t *d = reinterpret_cast<uint32_t *>(bins + rr * kTileStride + 16 * w);
+                    d[0] = pre[q].x; d[1] = pre[q].y; d[2] = pre[q].z; d[3] = pre[q].w;
+                }
             }
             __syncthreads();
+            fetch(t0 + kTileRows);
 #pragma unroll 1
             for (int it = 0; it < ITER; ++it) {
-                int node[kIlp];
-                const uint8_t *rowp[kIlp];
+                int node[ILP];
+                const uint8_t *rowp[ILP];
 #pragma unroll
-                for (int a = 0; a < kIlp; ++a) {
-                    const int row = wave * ROWS_PER_WAVE + (it * kIlp + a) * RPI + s;
+                for (int a = 0; a < ILP; ++a) {
+                    const int row = wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s;
                     rowp[a] = bins + row * kTileStride;
                     node[a] = 1;
                 }
 #pragma unroll
                 for (int l = 0; l < D; ++l) {
-                    uint32_t code[kIlp];
+                    uint32_t code[ILP];
 #pragma unroll
-                    for (int a = 0; a < kIlp; ++a) code[a] = nodes[node[a] * TC + t];
+                    for (int a = 0; a < ILP; ++a) code[a] = nodes[node[a] * TC + npos];
 #pragma unroll
-                    for (int a = 0; a < kIlp; ++a) {
-                        const uint32_t xb = rowp[a][code[a] & 0xffu];
-                        node[a] = 2 * node[a] + (xb > (code[a] >> 8) ? 1 : 0);
-                    }
+                    for (int a = 0; a < ILP; ++a) node[a] = descend(node[a], code[a], rowp[a][code[a] & 0xffu]);
                 }
 #pragma unroll
-                for (int a = 0; a < kIlp; ++a) {
-                    float v = leaves[(node[a] - NS) * TC + t];
-#pragma unroll
-                    for (int m = TC / 2; m > 0; m >>= 1) v += __shfl_xor(v, m, 64);
-                    if (t == 0) rowsum[wave * ROWS_PER_WAVE + (it * kIlp + a) * RPI + s] = v;
+                for (int a = 0; a < ILP; ++a) {
+                    const float v = group_total<TC>(leaves[(node[a] - NS) * TC + t]);
+                    if (t == TC - 1) rowsum[wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s] = v;
                 }
             }
             __syncthreads();
@@ -368,7 +440,7 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
                 v = v == 0.0f ? 0.0f : v;
                 const auto &u = U[fj];
                 const int rank = (int)(std::lower_bound(u.begin(), u.end(), v) - u.begin());
-                nodes[(n + 1) * g.tc + tt] = (uint16_t)(fj | (rank << 8));
+                nodes[(n + 1) * g.tc + node_pos(tt, g.tc)] = (uint16_t)(fj | (rank << 8));
             }
             for (int64_t l = 0; l <= n_int; ++l) leaves[l * g.tc + tt] = leaf[tree * (n_int + 1) + l];
         }

@@ -46,6 +46,10 @@ hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, con
 
 hipError_t launch_mlp(const hwsel_mlp_t &m, const float *X, int64_t R, int64_t ld, float *scores,
                       hipStream_t s);
+size_t mlp_packed_bytes();
+hipError_t launch_mlp_pack(const hwsel_mlp_t &m, void *packed, hipStream_t s);
+hipError_t launch_mlp_packed(const hwsel_mlp_t &m, const void *packed, const float *X, int64_t R, int64_t ld,
+                             float *scores, hipStream_t s);
 
 hipError_t launch_topk(const float *scores, const int64_t *seg, int32_t P, int32_t k, int32_t *idx,
                        float *vals, hipStream_t s);

@@ -1,9 +1,28 @@
 // Feed-forward ranker 128 -> 512 -> 512 -> 256 -> 1 (GELU, bf16 activations,
 // fp32 accumulation).
 //
-// Row-block kernel: a workgroup holds the activations of 16 rows in LDS and
-// walks the layers; each thread owns output units and reuses every weight it
-// loads across the 16 rows.
+// Unpacked path: a row-block kernel with fp32 FMAs (any weights, no
+// preparation).
+//
+// Packed path (weights arranged once by hwsel_mlp_pack): the hidden layers
+// run on the bf16 matrix cores, v_mfma_f32_32x32x16_bf16.
+//   * A workgroup (8 waves) owns a tile of 128 rows.  The tile's activations
+//     stay in LDS as bf16 for the whole network ([row][unit], rows padded by
+//     16 bytes so that the 16-byte fragment reads of 8 consecutive rows fall
+//     on 32 distinct banks); only X comes in and one score per row goes out.
+//   * Each layer is computed transposed, H_l^T = W_l * H_{l-1}^T: the A
+//     operand is weights, pre-arranged into MFMA fragment order so every
+//     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all); the B
+//     operand is 16 bytes of one activation row from LDS; the accumulator tile
+//     gives each lane 4 runs of 4 consecutive units of one row, which are
+//     written back as 8-byte LDS stores.
+//   * Waves split the output units of a layer, so every weight is read once
+//     per tile; a layer's results wait in registers until all waves have
+//     read the previous layer, then overwrite it in place.
+//   * GELU(a) = a/2 (1 + erf(a / sqrt 2)) with erf from Abramowitz & Stegun
+//     7.1.26 (|error| <= 1.5e-7, far below the bf16 rounding that follows).
+//   * The 256 -> 1 layer is a dot product folded into layer 3's epilogue,
+//     reduced across lanes and waves in a fixed order.
 #include "internal.hpp"
 
 #include <math.h>
@@ -11,9 +30,9 @@
 namespace hwsel {
 namespace {
 
-constexpr int kRows = 16;
-constexpr int kThreads = 256;
-
+// ---------------------------------------------------------------------------
+// Shared pieces
+// ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // Round fp32 to the nearest bf16 value (ties to even), kept in an fp32.
@@ -25,7 +44,34 @@ __device__ __forceinline__ float round_bf16(float v)
     return __uint_as_float(u & 0xffff0000u);
 }
 
-__device__ __forceinline__ float gelu(float a) { return 0.5f * a * (1.0f + erff(a * 0.70710678118654752f)); }
+__device__ __forceinline__ float gelu_exact(float a) { return 0.5f * a * (1.0f + erff(a * 0.70710678118654752f)); }
+
+// erf by Abramowitz & Stegun 7.1.26:
+//   erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
+//   t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7; odd extension for x < 0.
+__device__ __forceinline__ float gelu_as(float a)
+{
+    constexpr float p = 0.3275911f;
+    constexpr float a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f, a4 = -1.453152027f,
+                    a5 = 1.061405429f;
+    const float x = fabsf(a) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(p, x, 1.0f));
+    float poly = fmaf(a5, t, a4);
+    poly = fmaf(poly, t, a3);
+    poly = fmaf(poly, t, a2);
+    poly = fmaf(poly, t, a1);
+    poly *= t;
+    const float e = __builtin_amdgcn_exp2f(-1.44269504088896341f * x * x);
+    const float erf_abs = 1.0f - poly * e;
+    const float erf_v = a < 0.0f ? -erf_abs : erf_abs;
+    return 0.5f * a * (1.0f + erf_v);
+}
+
+// ---------------------------------------------------------------------------
+// Unpacked path
+// ---------------------------------------------------------------------------
+constexpr int kRows = 16;
+constexpr int kThreads = 256;
 
 template <int IN, int OUT>
 __device__ __forceinline__ void dense_gelu(const uint16_t *__restrict__ W, const float *__restrict__ b,
@@ -43,7 +89,7 @@ __device__ __forceinline__ void dense_gelu(const uint16_t *__restrict__ W, const
         }
         const float bu = b[u];
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) out[r][u] = round_bf16(gelu(acc[r] + bu));
+        for (int r = 0; r < kRows; ++r) out[r][u] = round_bf16(gelu_exact(acc[r] + bu));
     }
 }
 
@@ -70,13 +116,193 @@ __global__ __launch_bounds__(kThreads) void k_mlp_rows(hwsel_mlp_t m, const floa
     __syncthreads();
     dense_gelu<512, 256>(m.W3, m.b3, h2, h3);
     __syncthreads();
-    // output layer: 16 lanes per row
     const int r = threadIdx.x >> 4, part = threadIdx.x & 15;
     float acc = 0.0f;
     for (int j = part; j < 256; j += 16) acc = fmaf(bf16_to_f32(m.W4[j]), h3[r][j], acc);
 #pragma unroll
     for (int o = 8; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 16);
     if (part == 0 && row0 + r < R) scores[row0 + r] = acc + m.b4[0];
+}
+
+// ---------------------------------------------------------------------------
+// Packed path
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kTile = 128;                    // rows per workgroup
+constexpr int kMWaves = 8;
+constexpr int kHStride = 512 * 2 + 16;        // LDS bytes per activation row (512 units)
+constexpr int kH0Stride = 128 * 2 + 16;       // LDS bytes per input row (128 features)
+// fragment counts (32 units x 16 inputs each) per layer
+constexpr int kFrag1 = (512 / 32) * (128 / 16);
+constexpr int kFrag2 = (512 / 32) * (512 / 16);
+constexpr int kFrag3 = (256 / 32) * (512 / 16);
+constexpr size_t kPackedElems = (size_t)(kFrag1 + kFrag2 + kFrag3) * 512;
+
+// Fragment (mt, ks) of a [n_out][k_in] weight matrix: lane l, element e
+// holds W[32 mt + l % 32][16 ks + 8 (l / 32) + e].
+__global__ __launch_bounds__(256) void k_mlp_pack(const uint16_t *__restrict__ W1, const uint16_t *__restrict__ W2,
+                                                   const uint16_t *__restrict__ W3, uint16_t *__restrict__ out)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= (int64_t)kPackedElems) return;
+    int64_t idx = g;
+    const uint16_t *W;
+    int k_in;
+    if (idx < (int64_t)kFrag1 * 512) {
+        W = W1; k_in = 128;
+    } else if ((idx -= (int64_t)kFrag1 * 512) < (int64_t)kFrag2 * 512) {
+        W = W2; k_in = 512;
+    } else {
+        idx -= (int64_t)kFrag2 * 512;
+        W = W3; k_in = 512;
+    }
+    const int e = (int)(idx & 7), lane = (int)((idx >> 3) & 63);
+    const int64_t frag = idx >> 9;
+    const int ksteps = k_in / 16;
+    const int mt = (int)(frag / ksteps), ks = (int)(frag % ksteps);
+    out[g] = W[(int64_t)(32 * mt + (lane & 31)) * k_in + 16 * ks + 8 * (lane >> 5) + e];
+}
+
+// One hidden layer on the tile: H_out^T[units][rows] = W * H_in^T, GELU,
+// bf16.  Each wave computes MT x 32 units for all 128 rows.
+template <int K_IN, int MT>
+__device__ __forceinline__ void layer_mma(const bf16x8 *__restrict__ Wf, const uint8_t *h_in, int in_stride,
+                                          int unit0, int lane, f32x16 (&acc)[MT][4])
+{
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = f32x16{0.f};
+    constexpr int KS = K_IN / 16;
+    const int mt0 = unit0 / 32;
+    const int koff = 16 * (lane >> 5);               // byte offset of this lane's 8 inputs
+    const uint8_t *brow = h_in + (lane & 31) * in_stride + koff;
+#pragma unroll 2
+    for (int ks = 0; ks < KS; ++ks) {
+        bf16x8 a[MT], b[4];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) a[mt] = Wf[((int64_t)(mt0 + mt) * KS + ks) * 64 + lane];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+            b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * in_stride + ks * 32);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+    }
+}
+
+// Accumulator element v of tile (mt, nt) is unit 32 mt + 8 (v / 4) + 4 (lane / 32)
+// + v % 4 of row 32 nt + lane % 32.
+template <int MT>
+__device__ __forceinline__ void store_gelu(const f32x16 (&acc)[MT][4], const float *__restrict__ bias, int unit0,
+                                           int lane, uint8_t *h_out)
+{
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int u = unit0 + 32 * mt + 8 * g + 4 * (lane >> 5);
+            const float4 bb = *reinterpret_cast<const float4 *>(bias + u);
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                const int row = 32 * nt + (lane & 31);
+                const __bf16 y0 = (__bf16)gelu_as(acc[mt][nt][4 * g + 0] + bb.x);
+                const __bf16 y1 = (__bf16)gelu_as(acc[mt][nt][4 * g + 1] + bb.y);
+                const __bf16 y2 = (__bf16)gelu_as(acc[mt][nt][4 * g + 2] + bb.z);
+                const __bf16 y3 = (__bf16)gelu_as(acc[mt][nt][4 * g + 3] + bb.w);
+                const uint2 pk = make_uint2((uint32_t)__builtin_bit_cast(uint16_t, y0) |
+                                                ((uint32_t)__builtin_bit_cast(uint16_t, y1) << 16),
+                                            (uint32_t)__builtin_bit_cast(uint16_t, y2) |
+                                                ((uint32_t)__builtin_bit_cast(uint16_t, y3) << 16));
+                *reinterpret_cast<uint2 *>(h_out + row * kHStride + 2 * u) = pk;
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, const bf16x8 *__restrict__ packed,
+                                                              const float *__restrict__ X, int64_t R, int64_t ld,
+                                                              float *__restrict__ scores)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t h[kTile * kHStride];
+    __shared__ float red[kMWaves][kTile];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t row0 = (int64_t)blockIdx.x * kTile;
+
+    // input: standardise (fp32, two operations), NaN/inf read as 0, bf16
+    for (int e = threadIdx.x; e < kTile * 32; e += 64 * kMWaves) {
+        const int r = e >> 5, c4 = (e & 31) * 4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row0 + r < R) v = *reinterpret_cast<const float4 *>(X + (row0 + r) * ld + c4);
+        const float4 mu = *reinterpret_cast<const float4 *>(m.mean + c4);
+        const float4 is = *reinterpret_cast<const float4 *>(m.inv_std + c4);
+        const float xs[4] = {v.x, v.y, v.z, v.w}, ms[4] = {mu.x, mu.y, mu.z, mu.w}, ss[4] = {is.x, is.y, is.z, is.w};
+        uint16_t o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float xv = __builtin_isfinite(xs[q]) ? xs[q] : 0.0f;
+            const float centred = xv - ms[q];
+            o[q] = __builtin_bit_cast(uint16_t, (__bf16)(centred * ss[q]));
+        }
+        *reinterpret_cast<uint2 *>(h + r * kH0Stride + 2 * c4) =
+            make_uint2((uint32_t)o[0] | ((uint32_t)o[1] << 16), (uint32_t)o[2] | ((uint32_t)o[3] << 16));
+    }
+    __syncthreads();
+
+    const bf16x8 *W1f = packed;
+    const bf16x8 *W2f = W1f + kFrag1 * 64;
+    const bf16x8 *W3f = W2f + kFrag2 * 64;
+    {   // layer 1: 128 -> 512, 64 units per wave
+        f32x16 acc[2][4];
+        layer_mma<128, 2>(W1f, h, kH0Stride, 64 * wave, lane, acc);
+        __syncthreads();
+        store_gelu<2>(acc, m.b1, 64 * wave, lane, h);
+    }
+    __syncthreads();
+    {   // layer 2: 512 -> 512
+        f32x16 acc[2][4];
+        layer_mma<512, 2>(W2f, h, kHStride, 64 * wave, lane, acc);
+        __syncthreads();
+        store_gelu<2>(acc, m.b2, 64 * wave, lane, h);
+    }
+    __syncthreads();
+    {   // layer 3: 512 -> 256 (32 units per wave), then the 256 -> 1 dot product
+        f32x16 acc[1][4];
+        layer_mma<512, 1>(W3f, h, kHStride, 32 * wave, lane, acc);
+        float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int u = 32 * wave + 8 * g + 4 * (lane >> 5);
+            const float4 bb = *reinterpret_cast<const float4 *>(m.b3 + u);
+            const uint2 w4 = *reinterpret_cast<const uint2 *>(m.W4 + u);
+            const float wq[4] = {__uint_as_float(w4.x << 16), __uint_as_float(w4.x & 0xffff0000u),
+                                 __uint_as_float(w4.y << 16), __uint_as_float(w4.y & 0xffff0000u)};
+            const float bq[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float y = (float)(__bf16)gelu_as(acc[0][nt][4 * g + q] + bq[q]);
+                    part[nt] = fmaf(wq[q], y, part[nt]);
+                }
+        }
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const float other = __shfl_xor(part[nt], 32, 64);
+            if (lane < 32) red[wave][32 * nt + lane] = part[nt] + other;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < kTile && row0 + threadIdx.x < R) {
+        float s = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kMWaves; ++w) s += red[w][threadIdx.x];
+        scores[row0 + threadIdx.x] = s + m.b4[0];
+    }
 }
 
 }  // namespace
@@ -86,6 +312,23 @@ hipError_t launch_mlp(const hwsel_mlp_t &m, const float *X, int64_t R, int64_t l
 {
     const dim3 grid((unsigned)((R + kRows - 1) / kRows)), block(kThreads);
     hipLaunchKernelGGL(k_mlp_rows, grid, block, 0, s, m, X, R, ld, scores);
+    return hipGetLastError();
+}
+
+size_t mlp_packed_bytes() { return kPackedElems * sizeof(uint16_t); }
+
+hipError_t launch_mlp_pack(const hwsel_mlp_t &m, void *packed, hipStream_t s)
+{
+    const unsigned blocks = (unsigned)((kPackedElems + 255) / 256);
+    hipLaunchKernelGGL(k_mlp_pack, dim3(blocks), dim3(256), 0, s, m.W1, m.W2, m.W3, static_cast<uint16_t *>(packed));
+    return hipGetLastError();
+}
+
+hipError_t launch_mlp_packed(const hwsel_mlp_t &m, const void *packed, const float *X, int64_t R, int64_t ld,
+                             float *scores, hipStream_t s)
+{
+    const dim3 grid((unsigned)((R + kTile - 1) / kTile)), block(64 * kMWaves);
+    hipLaunchKernelGGL(k_mlp_mfma, grid, block, 0, s, m, static_cast<const bf16x8 *>(packed), X, R, ld, scores);
     return hipGetLastError();
 }
 

@@ -75,7 +75,9 @@ def lib() -> C.CDLL:
         L.hwsel_forest_pack.argtypes = [C.POINTER(hwsel_forest_t), vp, C.c_size_t, vp]
         L.hwsel_forest_workspace_bytes.argtypes = [C.POINTER(hwsel_forest_t), i64, C.POINTER(C.c_size_t)]
         L.hwsel_forest_leaves.argtypes = [C.POINTER(hwsel_forest_t), vp, i64, i64, vp, i64, vp, vp]
-        L.hwsel_mlp_score.argtypes = [C.POINTER(hwsel_mlp_t), vp, i64, i64, vp, vp]
+        L.hwsel_mlp_score.argtypes = [C.POINTER(hwsel_mlp_t), vp, vp, i64, i64, vp, vp]
+        L.hwsel_mlp_pack_bytes.argtypes = [C.POINTER(hwsel_mlp_t), C.POINTER(C.c_size_t)]
+        L.hwsel_mlp_pack.argtypes = [C.POINTER(hwsel_mlp_t), vp, C.c_size_t, vp]
         L.hwsel_topk_per_problem.argtypes = [vp, vp, i32, i32, vp, vp, vp]
         L.hwsel_regret.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp]
         _lib = L
@@ -217,14 +219,25 @@ def mlp_struct(m: dict) -> hwsel_mlp_t:
                                              ("mean", "inv_std", "W1", "W2", "W3", "W4", "b1", "b2", "b3", "b4")])
 
 
+def hwsel_mlp_pack(mlp: dict, packed: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Arrange W1..W3 once for the matrix-core kernel; returns the image."""
+    s = mlp_struct(mlp)
+    n = C.c_size_t(0)
+    _check("hwsel_mlp_pack_bytes", lib().hwsel_mlp_pack_bytes(C.byref(s), C.byref(n)))
+    if packed is None:
+        packed = torch.empty(int(n.value), dtype=torch.uint8, device=mlp["W1"].device)
+    _check("hwsel_mlp_pack", lib().hwsel_mlp_pack(C.byref(s), _ptr(packed), packed.numel(), _stream(stream)))
+    return packed
+
+
 def hwsel_mlp_score(mlp: dict, X: torch.Tensor, scores: torch.Tensor | None = None,
-                    stream=None) -> torch.Tensor:
+                    packed: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     R = X.shape[0]
     if scores is None:
         scores = torch.empty(R, dtype=torch.float32, device=X.device)
     s = mlp_struct(mlp)
-    _check("hwsel_mlp_score", lib().hwsel_mlp_score(C.byref(s), _ptr(X), R, X.stride(0), _ptr(scores),
-                                                    _stream(stream)))
+    _check("hwsel_mlp_score", lib().hwsel_mlp_score(C.byref(s), _ptr(packed), _ptr(X), R, X.stride(0),
+                                                    _ptr(scores), _stream(stream)))
     return scores
 
 

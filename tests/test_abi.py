@@ -85,13 +85,19 @@ def test_forest_leaves_rejects_empty_row_list(L):
 
 def test_mlp_rejects(L):
     m = hwsel.hwsel_mlp_t(128, 512, 512, 256, *([FAKE] * 10))
-    assert L.hwsel_mlp_score(C.byref(m), FAKE, 0, 128, FAKE, None) == 1
-    assert L.hwsel_mlp_score(C.byref(m), FAKE, 10, 100, FAKE, None) == 1
-    assert L.hwsel_mlp_score(C.byref(m), FAKE + 8, 10, 128, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m), None, FAKE, 0, 128, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m), None, FAKE, 10, 100, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m), None, FAKE + 8, 10, 128, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m), FAKE + 8, FAKE, 10, 128, FAKE, None) == 1    # misaligned image
     m2 = hwsel.hwsel_mlp_t(128, 256, 512, 256, *([FAKE] * 10))
-    assert L.hwsel_mlp_score(C.byref(m2), FAKE, 10, 128, FAKE, None) == 2
+    assert L.hwsel_mlp_score(C.byref(m2), None, FAKE, 10, 128, FAKE, None) == 2
     m3 = hwsel.hwsel_mlp_t(128, 512, 512, 256, *([FAKE] * 9), None)
-    assert L.hwsel_mlp_score(C.byref(m3), FAKE, 10, 128, FAKE, None) == 1
+    assert L.hwsel_mlp_score(C.byref(m3), None, FAKE, 10, 128, FAKE, None) == 1
+    n = C.c_size_t(0)
+    assert L.hwsel_mlp_pack_bytes(C.byref(m), C.byref(n)) == 0
+    assert n.value == 2 * (128 * 512 + 512 * 512 + 512 * 256)
+    assert L.hwsel_mlp_pack(C.byref(m), FAKE, n.value - 2, None) == 1
+    assert L.hwsel_mlp_pack(C.byref(m2), FAKE, n.value, None) == 2
 
 
 @pytest.mark.parametrize("P,k,status", [(0, 5, 1), (4, 0, 1), (4, 65, 1)])

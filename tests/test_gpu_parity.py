@@ -185,6 +185,15 @@ def test_forest_workload_full_size(name):
     say(f"  mean regret top1 {np.nanmean(o1):.4f}")
 
 
+def _assert_mlp(g, o):
+    rms = float(np.sqrt(np.mean(o.astype(np.float64) ** 2)))
+    err = np.abs(g.astype(np.float64) - o)
+    bound = 2e-2 * np.maximum(np.abs(o), rms)
+    i = int(np.argmax(err / bound))
+    assert np.all(err <= bound), f"row {i}: gpu {g[i]} oracle {o[i]} rms {rms}"
+    return float((err / bound).max()), rms
+
+
 def test_mlp_dataset_rows():
     say("mlp: features of the dataset-scale rows")
     w = synth.workload("mlp")
@@ -192,14 +201,45 @@ def test_mlp_dataset_rows():
     X = d.features(128)
     rows = synth.sample_rows(w.cfg, 8192)
     rows_d = torch.from_numpy(rows).cuda()
-    say("mlp: score all rows")
-    s = hwsel.hwsel_mlp_score(d.mlp, X)
+    say("mlp: matrix-core path on all rows (as benchmarked)")
+    packed = hwsel.hwsel_mlp_pack(d.mlp)
+    s = hwsel.hwsel_mlp_score(d.mlp, X, packed=packed)
     g = s.index_select(0, rows_d).cpu().numpy()
     Xs = X.index_select(0, rows_d).cpu().numpy()
     o = oracle.mlp(w.mlp, Xs)
-    rms = float(np.sqrt(np.mean(o.astype(np.float64) ** 2)))
-    err = np.abs(g.astype(np.float64) - o)
-    bound = 2e-2 * np.maximum(np.abs(o), rms)
-    say(f"  max err/bound {float((err / bound).max()):.3g}  rms {rms:.3g}")
-    assert np.all(err <= bound)
+    say("  max err/bound %.3g  rms %.3g" % _assert_mlp(g, o))
     assert bool(torch.isfinite(s).all())
+    s2 = hwsel.hwsel_mlp_score(d.mlp, X, packed=packed)
+    assert bool((s == s2).all())                                    # run-to-run identical
+    say("mlp: fp32 row-block path on the sample")
+    g2 = hwsel.hwsel_mlp_score(d.mlp, X.index_select(0, rows_d).contiguous()).cpu().numpy()
+    say("  max err/bound %.3g  rms %.3g" % _assert_mlp(g2, o))
+    # top-k on the MLP scores: admissible picks (oracle score within the tie band of the k-th)
+    idx, _ = hwsel.hwsel_topk_per_problem(s, d.seg, w.cfg.k)
+    idx = idx.cpu().numpy()
+    seg = w.seg
+    for p in range(0, w.cfg.n_problems, 75):
+        Xp = X[seg[p]:seg[p + 1]].cpu().numpy()
+        op = oracle.mlp(w.mlp, Xp)
+        kth = np.sort(op)[::-1][w.cfg.k - 1]
+        rms_p = float(np.sqrt(np.mean(op.astype(np.float64) ** 2)))
+        assert np.all(op[idx[p]] >= kth - 4e-2 * max(abs(kth), rms_p)), p
+
+
+@pytest.mark.parametrize("R", [1, 127, 129, 1000])
+def test_mlp_ragged_and_nonfinite(R):
+    say(f"mlp ragged R={R}")
+    rng = np.random.default_rng(R)
+    m = synth.mlp(synth.CONFIGS["mlp"])
+    md = {k: hwsel.to_device(v) for k, v in m.items()}
+    sd = np.where(m["inv_std"] > 0, 1.0 / np.where(m["inv_std"] > 0, m["inv_std"], 1.0), 1.0)
+    X = (rng.standard_normal((R, 128)) * sd + m["mean"]).astype(np.float32)
+    X[rng.random(X.shape) < 0.01] = np.nan
+    X[rng.random(X.shape) < 0.01] = np.inf
+    X[rng.random(X.shape) < 0.01] = -np.inf
+    Xd = torch.from_numpy(X).cuda()
+    o = oracle.mlp(m, X)
+    g = hwsel.hwsel_mlp_score(md, Xd, packed=hwsel.hwsel_mlp_pack(md)).cpu().numpy()
+    _assert_mlp(g, o)
+    g2 = hwsel.hwsel_mlp_score(md, Xd).cpu().numpy()
+    _assert_mlp(g2, o)
