@@ -37,6 +37,22 @@ LANE_OPS_PER_S = 256 * 64 * 2.4e9
 MIN_OPS_PER_VISIT = 4
 
 
+def forest_traffic_bytes():
+    """HBM bytes per hwsel_forest_score call on this workload, from the two
+    committed counter passes (FETCH_SIZE, WRITE_SIZE, scaled by the plain-copy
+    calibration) -- or None once the forest kernels have changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "forest_score_dataset_traffic.json")
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
+        return None
+    return 1024.0 * (rec["fetch_kib"] * rec["fetch_scale"] + rec["write_kib"] * rec["write_scale"])
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -72,6 +88,9 @@ def main():
     ap.add_argument("--cpu-problems", type=int, default=64,
                     help="problems in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="run one plain 1 GiB device-to-device copy before the timed region (a known-size "
+                         "reference for the HBM byte counters)")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {a.gpus}); "
@@ -131,6 +150,14 @@ def main():
         hwsel.hwsel_regret(rt, seg, outs[1][0], *regs[1])
         mark(7)
 
+    if a.calibration_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration copy: 1 GiB read + 1 GiB written")
+        del src, dst
     log(f"warmup {a.warmup}")
     for _ in range(a.warmup):
         step()
@@ -169,9 +196,10 @@ def main():
         "stages_ms": per_stage,
         "hbm_roofline_step": {"achieved": hbm_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                               "frac": hbm_gbs / HBM_PEAK_GBS, "bytes_per_row": step_bytes / R},
-        "roofline": {"kernel": "forest_score", "bound": "alu", "achieved": visit_rate / 1e9,
-                     "peak": peak_visits / 1e9, "unit": "Gvisits/s", "frac": visit_rate / peak_visits,
-                     "traffic": None, "visits_per_launch": visits,
+        "roofline": {"kernel": "hwsel_forest_score (k_bin + k_traverse<16,10> + k_reduce)", "bound": "alu",
+                     "achieved": visit_rate / 1e9, "peak": peak_visits / 1e9, "unit": "Gvisits/s",
+                     "frac": visit_rate / peak_visits, "traffic": forest_traffic_bytes(),
+                     "visits_per_launch": visits,
                      "hbm_frac": forest_bytes / t_forest / 1e9 / HBM_PEAK_GBS},
     }
     if not a.no_cpu_baseline:
