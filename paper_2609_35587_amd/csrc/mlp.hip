@@ -48,7 +48,8 @@ __device__ __forceinline__ float gelu_exact(float a) { return 0.5f * a * (1.0f +
 
 // erf by Abramowitz & Stegun 7.1.26:
 //   erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
-//   t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7; odd extension for x < 0.
+//   t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7.
+// With h = a/2 and erf odd: GELU(a) = h + |h| erf(|a| / sqrt 2).
 __device__ __forceinline__ float gelu_as(float a)
 {
     constexpr float p = 0.3275911f;
@@ -61,10 +62,10 @@ __device__ __forceinline__ float gelu_as(float a)
     poly = fmaf(poly, t, a2);
     poly = fmaf(poly, t, a1);
     poly *= t;
-    const float e = __builtin_amdgcn_exp2f(-1.44269504088896341f * x * x);
-    const float erf_abs = 1.0f - poly * e;
-    const float erf_v = a < 0.0f ? -erf_abs : erf_abs;
-    return 0.5f * a * (1.0f + erf_v);
+    const float e = __builtin_amdgcn_exp2f((x * -1.44269504088896341f) * x);
+    const float erf_abs = fmaf(-poly, e, 1.0f);
+    const float h = 0.5f * a;
+    return fmaf(fabsf(h), erf_abs, h);
 }
 
 // ---------------------------------------------------------------------------
@@ -165,63 +166,90 @@ __global__ __launch_bounds__(256) void k_mlp_pack(const uint16_t *__restrict__ W
     out[g] = W[(int64_t)(32 * mt + (lane & 31)) * k_in + 16 * ks + 8 * (lane >> 5) + e];
 }
 
-// One hidden layer on the tile: H_out^T[units][rows] = W * H_in^T, GELU,
-// bf16.  Each wave computes MT x 32 units for all 128 rows.
-template <int K_IN, int MT>
-__device__ __forceinline__ void layer_mma(const bf16x8 *__restrict__ Wf, const uint8_t *h_in, int in_stride,
-                                          int unit0, int lane, f32x16 (&acc)[MT][4])
+typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+typedef float f32x2_v __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to a pair of bf16 (round to nearest even), low half first.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = f32x16{0.f};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_v){lo, hi}, bf16x2_v));
+}
+
+constexpr int kPrefetch = 2;    // weight fragments in flight per wave
+
+// acc[nt] (+)= W-fragments of one 32-unit M-tile x activations of NB 32-row
+// N-tiles starting at row 32*nt0, over all K_IN inputs.  Weight fragments are
+// fetched kPrefetch k-steps ahead into a register ring.
+template <int K_IN, int NB>
+__device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const uint8_t *h_in, int in_stride,
+                                          int nt0, int lane, f32x16 (&acc)[NB])
+{
     constexpr int KS = K_IN / 16;
-    const int mt0 = unit0 / 32;
-    const int koff = 16 * (lane >> 5);               // byte offset of this lane's 8 inputs
-    const uint8_t *brow = h_in + (lane & 31) * in_stride + koff;
-#pragma unroll 2
+    constexpr int PF = kPrefetch < KS ? kPrefetch : KS;
+#pragma unroll
+    for (int nt = 0; nt < NB; ++nt) acc[nt] = f32x16{0.f};
+    const uint8_t *brow = h_in + ((lane & 31) + 32 * nt0) * in_stride + 16 * (lane >> 5);
+    bf16x8 ring[PF];
+#pragma unroll
+    for (int q = 0; q < PF; ++q) ring[q] = Wm[q * 64 + lane];
+#pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 a[MT], b[4];
+        bf16x8 b[NB];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) a[mt] = Wf[((int64_t)(mt0 + mt) * KS + ks) * 64 + lane];
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < NB; ++nt)
             b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * in_stride + ks * 32);
+        const bf16x8 a = ring[ks % PF];
+        if (ks + PF < KS) ring[ks % PF] = Wm[(ks + PF) * 64 + lane];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
-                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+        for (int nt = 0; nt < NB; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], acc[nt], 0, 0, 0);
     }
 }
 
-// Accumulator element v of tile (mt, nt) is unit 32 mt + 8 (v / 4) + 4 (lane / 32)
-// + v % 4 of row 32 nt + lane % 32.
-template <int MT>
-__device__ __forceinline__ void store_gelu(const f32x16 (&acc)[MT][4], const float *__restrict__ bias, int unit0,
-                                           int lane, uint8_t *h_out)
+// Accumulator element v of a tile is unit 8 (v / 4) + 4 (lane / 32) + v % 4
+// (plus the tile's first unit) of row (lane % 32) (plus the tile's first row).
+// GELU(acc + bias) rounded to bf16, 4 units packed per uint2.
+template <int NB>
+__device__ __forceinline__ void gelu_block(const f32x16 (&acc)[NB], const float *__restrict__ bias, int unit0,
+                                           int lane, uint2 (&out)[NB][4])
 {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
+    for (int g = 0; g < 4; ++g) {
+        const float4 bb = *reinterpret_cast<const float4 *>(bias + unit0 + 8 * g + 4 * (lane >> 5));
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int u = unit0 + 32 * mt + 8 * g + 4 * (lane >> 5);
-            const float4 bb = *reinterpret_cast<const float4 *>(bias + u);
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                const int row = 32 * nt + (lane & 31);
-                const __bf16 y0 = (__bf16)gelu_as(acc[mt][nt][4 * g + 0] + bb.x);
-                const __bf16 y1 = (__bf16)gelu_as(acc[mt][nt][4 * g + 1] + bb.y);
-                const __bf16 y2 = (__bf16)gelu_as(acc[mt][nt][4 * g + 2] + bb.z);
-                const __bf16 y3 = (__bf16)gelu_as(acc[mt][nt][4 * g + 3] + bb.w);
-                const uint2 pk = make_uint2((uint32_t)__builtin_bit_cast(uint16_t, y0) |
-                                                ((uint32_t)__builtin_bit_cast(uint16_t, y1) << 16),
-                                            (uint32_t)__builtin_bit_cast(uint16_t, y2) |
-                                                ((uint32_t)__builtin_bit_cast(uint16_t, y3) << 16));
-                *reinterpret_cast<uint2 *>(h_out + row * kHStride + 2 * u) = pk;
-            }
-        }
+        for (int nt = 0; nt < NB; ++nt)
+            out[nt][g] = make_uint2(pack_bf16x2(gelu_as(acc[nt][4 * g + 0] + bb.x), gelu_as(acc[nt][4 * g + 1] + bb.y)),
+                                    pack_bf16x2(gelu_as(acc[nt][4 * g + 2] + bb.z), gelu_as(acc[nt][4 * g + 3] + bb.w)));
     }
+}
+
+// A 512-unit hidden layer: each wave owns 64 units (two M-tiles), computed as
+// two blocks; GELU of a block runs right after its matrix products while the
+// other wave on the SIMD keeps the matrix core busy.  Results wait in
+// registers until every wave has finished reading the layer input.
+template <int K_IN>
+__device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const float *__restrict__ bias,
+                                          uint8_t *h, int in_stride, int wave, int lane)
+{
+    constexpr int KS = K_IN / 16;
+    uint2 staged[2][4][4];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+        f32x16 acc[4];
+        mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave + mt) * KS * 64, h, in_stride, 0, lane, acc);
+        gelu_block<4>(acc, bias, 64 * wave + 32 * mt, lane, staged[mt]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int row = 32 * nt + (lane & 31);
+                const int u = 64 * wave + 32 * mt + 8 * g + 4 * (lane >> 5);
+                *reinterpret_cast<uint2 *>(h + row * kHStride + 2 * u) = staged[mt][nt][g];
+            }
+    __syncthreads();
 }
 
 __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, const bf16x8 *__restrict__ packed,
@@ -240,40 +268,27 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
         if (row0 + r < R) v = *reinterpret_cast<const float4 *>(X + (row0 + r) * ld + c4);
         const float4 mu = *reinterpret_cast<const float4 *>(m.mean + c4);
         const float4 is = *reinterpret_cast<const float4 *>(m.inv_std + c4);
-        const float xs[4] = {v.x, v.y, v.z, v.w}, ms[4] = {mu.x, mu.y, mu.z, mu.w}, ss[4] = {is.x, is.y, is.z, is.w};
-        uint16_t o[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float xv = __builtin_isfinite(xs[q]) ? xs[q] : 0.0f;
-            const float centred = xv - ms[q];
-            o[q] = __builtin_bit_cast(uint16_t, (__bf16)(centred * ss[q]));
-        }
-        *reinterpret_cast<uint2 *>(h + r * kH0Stride + 2 * c4) =
-            make_uint2((uint32_t)o[0] | ((uint32_t)o[1] << 16), (uint32_t)o[2] | ((uint32_t)o[3] << 16));
+        const float z0 = ((__builtin_isfinite(v.x) ? v.x : 0.0f) - mu.x) * is.x;
+        const float z1 = ((__builtin_isfinite(v.y) ? v.y : 0.0f) - mu.y) * is.y;
+        const float z2 = ((__builtin_isfinite(v.z) ? v.z : 0.0f) - mu.z) * is.z;
+        const float z3 = ((__builtin_isfinite(v.w) ? v.w : 0.0f) - mu.w) * is.w;
+        *reinterpret_cast<uint2 *>(h + r * kH0Stride + 2 * c4) = make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
     }
     __syncthreads();
 
     const bf16x8 *W1f = packed;
     const bf16x8 *W2f = W1f + kFrag1 * 64;
     const bf16x8 *W3f = W2f + kFrag2 * 64;
-    {   // layer 1: 128 -> 512, 64 units per wave
-        f32x16 acc[2][4];
-        layer_mma<128, 2>(W1f, h, kH0Stride, 64 * wave, lane, acc);
-        __syncthreads();
-        store_gelu<2>(acc, m.b1, 64 * wave, lane, h);
-    }
-    __syncthreads();
-    {   // layer 2: 512 -> 512
-        f32x16 acc[2][4];
-        layer_mma<512, 2>(W2f, h, kHStride, 64 * wave, lane, acc);
-        __syncthreads();
-        store_gelu<2>(acc, m.b2, 64 * wave, lane, h);
-    }
-    __syncthreads();
-    {   // layer 3: 512 -> 256 (32 units per wave), then the 256 -> 1 dot product
-        f32x16 acc[1][4];
-        layer_mma<512, 1>(W3f, h, kHStride, 32 * wave, lane, acc);
-        float part[4] = {0.f, 0.f, 0.f, 0.f};
+    hidden512<128>(W1f, m.b1, h, kH0Stride, wave, lane);     // layer 1: 128 -> 512
+    hidden512<512>(W2f, m.b2, h, kHStride, wave, lane);      // layer 2: 512 -> 512
+
+    // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two N-tiles),
+    // folded with the 256 -> 1 dot product
+    float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+        f32x16 acc[2];
+        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, h, kHStride, 2 * blk, lane, acc);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int u = 32 * wave + 8 * g + 4 * (lane >> 5);
@@ -283,18 +298,18 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
                                  __uint_as_float(w4.y << 16), __uint_as_float(w4.y & 0xffff0000u)};
             const float bq[4] = {bb.x, bb.y, bb.z, bb.w};
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const float y = (float)(__bf16)gelu_as(acc[0][nt][4 * g + q] + bq[q]);
-                    part[nt] = fmaf(wq[q], y, part[nt]);
+                    const float y = (float)(__bf16)gelu_as(acc[nt][4 * g + q] + bq[q]);
+                    part[2 * blk + nt] = fmaf(wq[q], y, part[2 * blk + nt]);
                 }
         }
+    }
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            const float other = __shfl_xor(part[nt], 32, 64);
-            if (lane < 32) red[wave][32 * nt + lane] = part[nt] + other;
-        }
+    for (int nt = 0; nt < 4; ++nt) {
+        const float other = __shfl_xor(part[nt], 32, 64);
+        if (lane < 32) red[wave][32 * nt + lane] = part[nt] + other;
     }
     __syncthreads();
     if (threadIdx.x < kTile && row0 + threadIdx.x < R) {
