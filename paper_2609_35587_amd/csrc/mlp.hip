@@ -27,6 +27,8 @@
 
 #include <math.h>
 
+#include <utility>
+
 namespace hwsel {
 namespace {
 
@@ -133,8 +135,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kTile = 128;                    // rows per workgroup
 constexpr int kMWaves = 8;
-constexpr int kHStride = 512 * 2 + 16;        // LDS bytes per activation row (512 units)
-constexpr int kH0Stride = 128 * 2 + 16;       // LDS bytes per input row (128 features)
+constexpr int kActBytes = kTile * 1024;       // 128 rows x 512 bf16 units
+constexpr int kRingBytes = 4 * 1024;          // per wave: four 1 KB weight fragments
+constexpr int kLdsBytes = kActBytes + kMWaves * kRingBytes;   // 160 KB
 // fragment counts (32 units x 16 inputs each) per layer
 constexpr int kFrag1 = (512 / 32) * (128 / 16);
 constexpr int kFrag2 = (512 / 32) * (512 / 16);
@@ -175,68 +178,130 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_v){lo, hi}, bf16x2_v));
 }
 
-constexpr int kPrefetch = 2;    // weight fragments in flight per wave
+// Activation rows live in LDS unpadded; the 16-byte chunk j of row r is
+// stored at chunk j ^ (r % 8), so the 16-byte fragment reads of 8 consecutive
+// rows at the same logical chunk hit 8 distinct 16-byte bank groups.
+__device__ __forceinline__ int act_offset(int row, int row_bytes, int unit)
+{
+    return row * row_bytes + ((((unit >> 3) ^ row) & 7) | ((unit >> 3) & ~7)) * 16 + (unit & 7) * 2;
+}
 
-// acc[nt] (+)= W-fragments of one 32-unit M-tile x activations of NB 32-row
-// N-tiles starting at row 32*nt0, over all K_IN inputs.  Weight fragments are
-// fetched kPrefetch k-steps ahead into a register ring.
+__device__ __forceinline__ uint32_t lds_address(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// Copy 16 bytes per lane from global memory straight into LDS at
+// lds_base + 16 * lane (one weight fragment per wave).  M0 carries the LDS
+// address and is restored afterwards.
+__device__ __forceinline__ void dma_fragment(const bf16x8 *g, uint32_t lds_base)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %1\n\t"
+                 "global_load_lds_dwordx4 %2, off\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(lds_base), "v"(g)
+                 : "memory");
+}
+
+// Loads complete in issue order; "at most N outstanding" means every load
+// older than the N most recent has landed (other loads in flight only make
+// this stricter).  The memory clobber keeps LDS reads after the wait.
+template <int N>
+__device__ __forceinline__ void fragments_landed()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
+}
+
+// A ring slot may be refilled once this wave's reads of it have completed.
+__device__ __forceinline__ void reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
+
+// acc[nt] = sum over K_IN of W-fragments of one 32-unit M-tile x activations
+// of NB 32-row N-tiles starting at row 32*nt0.  The weight fragments stream
+// through the wave's 4-slot LDS ring, two k-steps ahead; the k loop is rolled,
+// four k-steps per trip.
 template <int K_IN, int NB>
-__device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const uint8_t *h_in, int in_stride,
-                                          int nt0, int lane, f32x16 (&acc)[NB])
+__device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const uint8_t *act, int row_bytes,
+                                          int nt0, int lane, uint32_t ring, const uint8_t *ring_ptr,
+                                          f32x16 (&acc)[NB])
 {
     constexpr int KS = K_IN / 16;
-    constexpr int PF = kPrefetch < KS ? kPrefetch : KS;
+    static_assert(KS % 4 == 0, "k loop");
 #pragma unroll
     for (int nt = 0; nt < NB; ++nt) acc[nt] = f32x16{0.f};
-    const uint8_t *brow = h_in + ((lane & 31) + 32 * nt0) * in_stride + 16 * (lane >> 5);
-    bf16x8 ring[PF];
-#pragma unroll
-    for (int q = 0; q < PF; ++q) ring[q] = Wm[q * 64 + lane];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    const int r0 = (lane & 31) + 32 * nt0;
+    const uint8_t *brow = act + r0 * row_bytes;
+    const int sw = lane & 7, half = lane >> 5;
+    const bf16x8 *wp = Wm + lane;
+    auto step = [&](int slot, int ks) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
+        const int chunk = (((2 * ks + half) ^ sw) & 7) | ((2 * ks + half) & ~7);
         bf16x8 b[NB];
 #pragma unroll
         for (int nt = 0; nt < NB; ++nt)
-            b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * in_stride + ks * 32);
-        const bf16x8 a = ring[ks % PF];
-        if (ks + PF < KS) ring[ks % PF] = Wm[(ks + PF) * 64 + lane];
+            b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
 #pragma unroll
         for (int nt = 0; nt < NB; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], acc[nt], 0, 0, 0);
+    };
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dma_fragment(wp + q * 64, ring + q * 1024);
+    fragments_landed<2>();
+#pragma unroll 1
+    for (int ks = 0; ks < KS; ks += 4) {
+        step(0, ks);
+        step(1, ks + 1);
+        const bool more = ks + 4 < KS;
+        if (more) {
+            reads_done();
+            dma_fragment(wp + (ks + 4) * 64, ring);
+            dma_fragment(wp + (ks + 5) * 64, ring + 1024);
+            fragments_landed<2>();
+        } else {
+            fragments_landed<0>();
+        }
+        step(2, ks + 2);
+        step(3, ks + 3);
+        if (more) {
+            reads_done();
+            dma_fragment(wp + (ks + 6) * 64, ring + 2048);
+            dma_fragment(wp + (ks + 7) * 64, ring + 3072);
+            fragments_landed<2>();
+        }
     }
 }
 
-// Accumulator element v of a tile is unit 8 (v / 4) + 4 (lane / 32) + v % 4
-// (plus the tile's first unit) of row (lane % 32) (plus the tile's first row).
-// GELU(acc + bias) rounded to bf16, 4 units packed per uint2.
-template <int NB>
-__device__ __forceinline__ void gelu_block(const f32x16 (&acc)[NB], const float *__restrict__ bias, int unit0,
-                                           int lane, uint2 (&out)[NB][4])
+// GELU(acc + bias) of one group (4 consecutive units of one row) of an
+// accumulator tile, rounded to bf16 and packed.  Accumulator element v of a
+// tile is unit 8 (v / 4) + 4 (lane / 32) + v % 4 (plus the tile's first unit)
+// of row lane % 32 (plus the tile's first row).
+__device__ __forceinline__ uint2 gelu_group(const f32x16 &acc, int g, const float4 &bb)
 {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        const float4 bb = *reinterpret_cast<const float4 *>(bias + unit0 + 8 * g + 4 * (lane >> 5));
-#pragma unroll
-        for (int nt = 0; nt < NB; ++nt)
-            out[nt][g] = make_uint2(pack_bf16x2(gelu_as(acc[nt][4 * g + 0] + bb.x), gelu_as(acc[nt][4 * g + 1] + bb.y)),
-                                    pack_bf16x2(gelu_as(acc[nt][4 * g + 2] + bb.z), gelu_as(acc[nt][4 * g + 3] + bb.w)));
-    }
+    return make_uint2(pack_bf16x2(gelu_as(acc[4 * g + 0] + bb.x), gelu_as(acc[4 * g + 1] + bb.y)),
+                      pack_bf16x2(gelu_as(acc[4 * g + 2] + bb.z), gelu_as(acc[4 * g + 3] + bb.w)));
 }
 
-// A 512-unit hidden layer: each wave owns 64 units (two M-tiles), computed as
-// two blocks; GELU of a block runs right after its matrix products while the
-// other wave on the SIMD keeps the matrix core busy.  Results wait in
-// registers until every wave has finished reading the layer input.
+// A 512-unit hidden layer: each wave owns 64 units (two M-tiles) for all 128
+// rows.  Results wait in registers until every wave has finished reading the
+// layer input, then overwrite it in place.
 template <int K_IN>
 __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const float *__restrict__ bias,
-                                          uint8_t *h, int in_stride, int wave, int lane)
+                                          uint8_t *act, int in_row_bytes, int wave, int lane, uint32_t ring,
+                                          const uint8_t *ring_ptr)
 {
     constexpr int KS = K_IN / 16;
     uint2 staged[2][4][4];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
         f32x16 acc[4];
-        mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave + mt) * KS * 64, h, in_stride, 0, lane, acc);
-        gelu_block<4>(acc, bias, 64 * wave + 32 * mt, lane, staged[mt]);
+        mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave + mt) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr, acc);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 bb = *reinterpret_cast<const float4 *>(bias + 64 * wave + 32 * mt + 8 * g + 4 * (lane >> 5));
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) staged[mt][nt][g] = gelu_group(acc[nt], g, bb);
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -247,7 +312,7 @@ __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const f
             for (int g = 0; g < 4; ++g) {
                 const int row = 32 * nt + (lane & 31);
                 const int u = 64 * wave + 32 * mt + 8 * g + 4 * (lane >> 5);
-                *reinterpret_cast<uint2 *>(h + row * kHStride + 2 * u) = staged[mt][nt][g];
+                *reinterpret_cast<uint2 *>(act + act_offset(row, 1024, u)) = staged[mt][nt][g];
             }
     __syncthreads();
 }
@@ -256,9 +321,11 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
                                                               const float *__restrict__ X, int64_t R, int64_t ld,
                                                               float *__restrict__ scores)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t h[kTile * kHStride];
-    __shared__ float red[kMWaves][kTile];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
+    uint8_t *act = lds;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint8_t *ring_ptr = lds + kActBytes + wave * kRingBytes;
+    const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_address(ring_ptr));
     const int64_t row0 = (int64_t)blockIdx.x * kTile;
 
     // input: standardise (fp32, two operations), NaN/inf read as 0, bf16
@@ -272,50 +339,53 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
         const float z1 = ((__builtin_isfinite(v.y) ? v.y : 0.0f) - mu.y) * is.y;
         const float z2 = ((__builtin_isfinite(v.z) ? v.z : 0.0f) - mu.z) * is.z;
         const float z3 = ((__builtin_isfinite(v.w) ? v.w : 0.0f) - mu.w) * is.w;
-        *reinterpret_cast<uint2 *>(h + r * kH0Stride + 2 * c4) = make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
+        *reinterpret_cast<uint2 *>(act + act_offset(r, 256, c4)) = make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
     }
     __syncthreads();
 
     const bf16x8 *W1f = packed;
     const bf16x8 *W2f = W1f + kFrag1 * 64;
     const bf16x8 *W3f = W2f + kFrag2 * 64;
-    hidden512<128>(W1f, m.b1, h, kH0Stride, wave, lane);     // layer 1: 128 -> 512
-    hidden512<512>(W2f, m.b2, h, kHStride, wave, lane);      // layer 2: 512 -> 512
+    hidden512<128>(W1f, m.b1, act, 256, wave, lane, ring, ring_ptr);     // layer 1: 128 -> 512
+    hidden512<512>(W2f, m.b2, act, 1024, wave, lane, ring, ring_ptr);    // layer 2: 512 -> 512
 
     // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two N-tiles),
-    // folded with the 256 -> 1 dot product
+    // GELU, bf16, then the 256 -> 1 dot product
     float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
         f32x16 acc[2];
-        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, h, kHStride, 2 * blk, lane, acc);
+        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2 * blk, lane, ring, ring_ptr, acc);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int u = 32 * wave + 8 * g + 4 * (lane >> 5);
             const float4 bb = *reinterpret_cast<const float4 *>(m.b3 + u);
-            const uint2 w4 = *reinterpret_cast<const uint2 *>(m.W4 + u);
-            const float wq[4] = {__uint_as_float(w4.x << 16), __uint_as_float(w4.x & 0xffff0000u),
-                                 __uint_as_float(w4.y << 16), __uint_as_float(w4.y & 0xffff0000u)};
-            const float bq[4] = {bb.x, bb.y, bb.z, bb.w};
+            const uint2 w = *reinterpret_cast<const uint2 *>(m.W4 + u);
 #pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const float y = (float)(__bf16)gelu_as(acc[nt][4 * g + q] + bq[q]);
-                    part[2 * blk + nt] = fmaf(wq[q], y, part[2 * blk + nt]);
-                }
+            for (int nt = 0; nt < 2; ++nt) {
+                const uint2 y = gelu_group(acc[nt], g, bb);
+                float p = part[2 * blk + nt];
+                p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
+                p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
+                p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
+                p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
+                part[2 * blk + nt] = p;
+            }
         }
     }
+    // per-row partial sums: lanes l and l + 32 hold the same row; the wave's
+    // slot of the (now idle) fragment ring collects them
+    float *red = reinterpret_cast<float *>(lds + kActBytes);      // [wave][128], inside each wave's own ring
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
         const float other = __shfl_xor(part[nt], 32, 64);
-        if (lane < 32) red[wave][32 * nt + lane] = part[nt] + other;
+        if (lane < 32) red[wave * (kRingBytes / 4) + 32 * nt + lane] = part[nt] + other;
     }
     __syncthreads();
     if (threadIdx.x < kTile && row0 + threadIdx.x < R) {
         float s = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kMWaves; ++w) s += red[w][threadIdx.x];
+        for (int w = 0; w < kMWaves; ++w) s += red[w * (kRingBytes / 4) + threadIdx.x];
         scores[row0 + threadIdx.x] = s + m.b4[0];
     }
 }
