@@ -48,26 +48,30 @@ __device__ __forceinline__ float round_bf16(float v)
 
 __device__ __forceinline__ float gelu_exact(float a) { return 0.5f * a * (1.0f + erff(a * 0.70710678118654752f)); }
 
-// erf by Abramowitz & Stegun 7.1.26:
-//   erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
-//   t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7.
-// With h = a/2 and erf odd: GELU(a) = h + |h| erf(|a| / sqrt 2).
+// GELU from the erf approximation of Abramowitz & Stegun 7.1.28:
+//   erf(x) = 1 - P(x)^-16,  P(x) = 1 + a1 x + ... + a6 x^6,  x >= 0,
+//   |error| <= 3e-7.
+// GELU(a) = a/2 (1 + erf(a / sqrt 2)) = max(a, 0) - |a|/2 P(|a| / sqrt 2)^-16.
+// The coefficients below are 2^(1/16) a_i / 2^(i/2), so Q(|a|)^16 =
+// 2 P(|a| / sqrt 2)^16 and one reciprocal gives the |a|/2 factor's 1/2.
+// Q^16 overflows to +inf for |a| > ~19, where the reciprocal is 0 and the
+// result max(a, 0) is exact in fp32.
 __device__ __forceinline__ float gelu_as(float a)
 {
-    constexpr float p = 0.3275911f;
-    constexpr float a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f, a4 = -1.453152027f,
-                    a5 = 1.061405429f;
-    const float x = fabsf(a) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(p, x, 1.0f));
-    float poly = fmaf(a5, t, a4);
-    poly = fmaf(poly, t, a3);
-    poly = fmaf(poly, t, a2);
-    poly = fmaf(poly, t, a1);
-    poly *= t;
-    const float e = __builtin_amdgcn_exp2f((x * -1.44269504088896341f) * x);
-    const float erf_abs = fmaf(-poly, e, 1.0f);
-    const float h = 0.5f * a;
-    return fmaf(fabsf(h), erf_abs, h);
+    constexpr float c0 = 1.0442737824274138f, c1 = 0.052075163f, c2 = 0.022076998f, c3 = 0.0034227392f,
+                    c4 = 3.9686137e-05f, c5 = 5.1055209e-05f, c6 = 5.6212997e-06f;
+    const float x = fabsf(a);
+    float q = fmaf(c6, x, c5);
+    q = fmaf(q, x, c4);
+    q = fmaf(q, x, c3);
+    q = fmaf(q, x, c2);
+    q = fmaf(q, x, c1);
+    q = fmaf(q, x, c0);
+    q *= q;
+    q *= q;
+    q *= q;
+    q *= q;
+    return fmaf(-x, __builtin_amdgcn_rcpf(q), fmaxf(a, 0.0f));
 }
 
 // ---------------------------------------------------------------------------
@@ -218,68 +222,95 @@ __device__ __forceinline__ void fragments_landed()
 // A ring slot may be refilled once this wave's reads of it have completed.
 __device__ __forceinline__ void reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
 
-// acc[nt] = sum over K_IN of W-fragments of one 32-unit M-tile x activations
-// of NB 32-row N-tiles starting at row 32*nt0.  The weight fragments stream
-// through the wave's 4-slot LDS ring, two k-steps ahead; the k loop is rolled,
-// four k-steps per trip.
+// acc[nt] = init + sum over K_IN of W-fragments of one 32-unit M-tile x
+// activations of NB 32-row N-tiles starting at row 32*nt0.  `init` (the
+// bias in accumulator layout) enters as the first product's addend.  The
+// weight fragments stream through the wave's 4-slot LDS ring, two k-steps
+// ahead; the k loop is rolled, four k-steps per trip, after a peeled first
+// trip.
 template <int K_IN, int NB>
 __device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const uint8_t *act, int row_bytes,
                                           int nt0, int lane, uint32_t ring, const uint8_t *ring_ptr,
-                                          f32x16 (&acc)[NB])
+                                          const f32x16 &init, f32x16 (&acc)[NB])
 {
     constexpr int KS = K_IN / 16;
     static_assert(KS % 4 == 0, "k loop");
-#pragma unroll
-    for (int nt = 0; nt < NB; ++nt) acc[nt] = f32x16{0.f};
     const int r0 = (lane & 31) + 32 * nt0;
     const uint8_t *brow = act + r0 * row_bytes;
     const int sw = lane & 7, half = lane >> 5;
     const bf16x8 *wp = Wm + lane;
-    auto step = [&](int slot, int ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
+    auto load = [&](int slot, int ks, bf16x8 &a, bf16x8 (&b)[NB]) {
+        a = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
         const int chunk = (((2 * ks + half) ^ sw) & 7) | ((2 * ks + half) & ~7);
-        bf16x8 b[NB];
 #pragma unroll
         for (int nt = 0; nt < NB; ++nt)
             b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
+    };
+    auto step = [&](int slot, int ks) {
+        bf16x8 a, b[NB];
+        load(slot, ks, a, b);
 #pragma unroll
         for (int nt = 0; nt < NB; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], acc[nt], 0, 0, 0);
+    };
+    // refill after k-steps ks, ks+1 of a trip (slots 0, 1) or ks+2, ks+3 (slots 2, 3)
+    auto refill = [&](int first_slot, int ks_next) {
+        if (ks_next < KS) {
+            reads_done();
+            dma_fragment(wp + ks_next * 64, ring + first_slot * 1024);
+            dma_fragment(wp + (ks_next + 1) * 64, ring + (first_slot + 1) * 1024);
+            fragments_landed<2>();
+        } else if (first_slot == 0) {
+            fragments_landed<0>();
+        }
     };
 #pragma unroll
     for (int q = 0; q < 4; ++q) dma_fragment(wp + q * 64, ring + q * 1024);
     fragments_landed<2>();
+    {   // first trip: the first product adds the bias
+        bf16x8 a, b[NB];
+        load(0, 0, a, b);
+#pragma unroll
+        for (int nt = 0; nt < NB; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], init, 0, 0, 0);
+        step(1, 1);
+        refill(0, 4);
+        step(2, 2);
+        step(3, 3);
+        refill(2, 6);
+    }
 #pragma unroll 1
-    for (int ks = 0; ks < KS; ks += 4) {
+    for (int ks = 4; ks < KS; ks += 4) {
         step(0, ks);
         step(1, ks + 1);
-        const bool more = ks + 4 < KS;
-        if (more) {
-            reads_done();
-            dma_fragment(wp + (ks + 4) * 64, ring);
-            dma_fragment(wp + (ks + 5) * 64, ring + 1024);
-            fragments_landed<2>();
-        } else {
-            fragments_landed<0>();
-        }
+        refill(0, ks + 4);
         step(2, ks + 2);
         step(3, ks + 3);
-        if (more) {
-            reads_done();
-            dma_fragment(wp + (ks + 6) * 64, ring + 2048);
-            dma_fragment(wp + (ks + 7) * 64, ring + 3072);
-            fragments_landed<2>();
-        }
+        refill(2, ks + 6);
     }
 }
 
-// GELU(acc + bias) of one group (4 consecutive units of one row) of an
-// accumulator tile, rounded to bf16 and packed.  Accumulator element v of a
-// tile is unit 8 (v / 4) + 4 (lane / 32) + v % 4 (plus the tile's first unit)
-// of row lane % 32 (plus the tile's first row).
-__device__ __forceinline__ uint2 gelu_group(const f32x16 &acc, int g, const float4 &bb)
+// Bias of one 32-unit M-tile starting at unit u0, in accumulator layout.
+__device__ __forceinline__ f32x16 bias_tile(const float *__restrict__ bias, int u0, int lane)
 {
-    return make_uint2(pack_bf16x2(gelu_as(acc[4 * g + 0] + bb.x), gelu_as(acc[4 * g + 1] + bb.y)),
-                      pack_bf16x2(gelu_as(acc[4 * g + 2] + bb.z), gelu_as(acc[4 * g + 3] + bb.w)));
+    f32x16 v;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const float4 b = *reinterpret_cast<const float4 *>(bias + u0 + 8 * g + 4 * (lane >> 5));
+        v[4 * g + 0] = b.x;
+        v[4 * g + 1] = b.y;
+        v[4 * g + 2] = b.z;
+        v[4 * g + 3] = b.w;
+    }
+    return v;
+}
+
+// GELU of one group (4 consecutive units of one row) of an accumulator
+// tile, rounded to bf16 and packed.  Accumulator element v of a tile is unit
+// 8 (v / 4) + 4 (lane / 32) + v % 4 (plus the tile's first unit) of row
+// lane % 32 (plus the tile's first row).
+__device__ __forceinline__ uint2 gelu_group(const f32x16 &acc, int g)
+{
+    return make_uint2(pack_bf16x2(gelu_as(acc[4 * g + 0]), gelu_as(acc[4 * g + 1])),
+                      pack_bf16x2(gelu_as(acc[4 * g + 2]), gelu_as(acc[4 * g + 3])));
 }
 
 // A 512-unit hidden layer: each wave owns 64 units (two M-tiles) for all 128
@@ -295,13 +326,12 @@ __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const f
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
         f32x16 acc[4];
-        mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave + mt) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr, acc);
+        mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave + mt) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr,
+                           bias_tile(bias, 64 * wave + 32 * mt, lane), acc);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const float4 bb = *reinterpret_cast<const float4 *>(bias + 64 * wave + 32 * mt + 8 * g + 4 * (lane >> 5));
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) staged[mt][nt][g] = gelu_group(acc[nt], g, bb);
-        }
+            for (int nt = 0; nt < 4; ++nt) staged[mt][nt][g] = gelu_group(acc[nt], g);
     }
     __syncthreads();
 #pragma unroll
@@ -355,15 +385,15 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
         f32x16 acc[2];
-        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2 * blk, lane, ring, ring_ptr, acc);
+        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2 * blk, lane, ring, ring_ptr,
+                          bias_tile(m.b3, 32 * wave, lane), acc);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int u = 32 * wave + 8 * g + 4 * (lane >> 5);
-            const float4 bb = *reinterpret_cast<const float4 *>(m.b3 + u);
             const uint2 w = *reinterpret_cast<const uint2 *>(m.W4 + u);
 #pragma unroll
             for (int nt = 0; nt < 2; ++nt) {
-                const uint2 y = gelu_group(acc[nt], g, bb);
+                const uint2 y = gelu_group(acc[nt], g);
                 float p = part[2 * blk + nt];
                 p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
                 p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
