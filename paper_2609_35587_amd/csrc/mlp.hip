@@ -7,20 +7,23 @@
 // Packed path (weights arranged once by hwsel_mlp_pack): the hidden layers
 // run on the bf16 matrix cores, v_mfma_f32_32x32x16_bf16.
 //   * A workgroup (8 waves) owns a tile of 128 rows.  The tile's activations
-//     stay in LDS as bf16 for the whole network ([row][unit], rows padded by
-//     16 bytes so that the 16-byte fragment reads of 8 consecutive rows fall
-//     on 32 distinct banks); only X comes in and one score per row goes out.
+//     stay in LDS as bf16 for the whole network ([row][unit], 16-byte chunks
+//     XOR-swizzled by row so that 16 consecutive rows at one logical chunk
+//     fall on 16 distinct 16-byte bank groups); only X comes in and one score
+//     per row goes out.
 //   * Each layer is computed transposed, H_l^T = W_l * H_{l-1}^T: the A
 //     operand is weights, pre-arranged into MFMA fragment order so every
-//     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all); the B
-//     operand is 16 bytes of one activation row from LDS; the accumulator tile
-//     gives each lane 4 runs of 4 consecutive units of one row, which are
-//     written back as 8-byte LDS stores.
+//     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all), sent
+//     by DMA loads straight into a 4-slot LDS ring per wave; the B operand is
+//     16 bytes of one activation row from LDS; the accumulator tile gives each
+//     lane 4 runs of 4 consecutive units of one row.
 //   * Waves split the output units of a layer, so every weight is read once
 //     per tile; a layer's results wait in registers until all waves have
-//     read the previous layer, then overwrite it in place.
+//     read the previous layer, then overwrite it in place.  While a wave's
+//     second block of products runs on the matrix core, the vector units
+//     finish the first block's epilogue.
 //   * GELU(a) = a/2 (1 + erf(a / sqrt 2)) with erf from Abramowitz & Stegun
-//     7.1.26 (|error| <= 1.5e-7, far below the bf16 rounding that follows).
+//     7.1.28 (|error| <= 3e-7, far below the bf16 rounding that follows).
 //   * The 256 -> 1 layer is a dot product folded into layer 3's epilogue,
 //     reduced across lanes and waves in a fixed order.
 #include "internal.hpp"
@@ -183,11 +186,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 }
 
 // Activation rows live in LDS unpadded; the 16-byte chunk j of row r is
-// stored at chunk j ^ (r % 8), so the 16-byte fragment reads of 8 consecutive
-// rows at the same logical chunk hit 8 distinct 16-byte bank groups.
+// stored at chunk j ^ (r % 16) (within its aligned group of 16 chunks).  The
+// 64 banks of LDS serve a 16-byte access of 16 lanes per cycle, and the 16
+// lanes of such a group read or write 16 consecutive rows at the same logical
+// chunk, which this places on 16 distinct 16-byte bank groups.
 __device__ __forceinline__ int act_offset(int row, int row_bytes, int unit)
 {
-    return row * row_bytes + ((((unit >> 3) ^ row) & 7) | ((unit >> 3) & ~7)) * 16 + (unit & 7) * 2;
+    return row * row_bytes + ((((unit >> 3) ^ row) & 15) | ((unit >> 3) & ~15)) * 16 + (unit & 7) * 2;
 }
 
 __device__ __forceinline__ uint32_t lds_address(const void *p)
@@ -222,37 +227,42 @@ __device__ __forceinline__ void fragments_landed()
 // A ring slot may be refilled once this wave's reads of it have completed.
 __device__ __forceinline__ void reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
 
+struct NoSide {
+    __device__ void operator()(int) const {}
+};
+
 // acc[nt] = init + sum over K_IN of W-fragments of one 32-unit M-tile x
 // activations of NB 32-row N-tiles starting at row 32*nt0.  `init` (the
 // bias in accumulator layout) enters as the first product's addend.  The
 // weight fragments stream through the wave's 4-slot LDS ring, two k-steps
-// ahead; the k loop is rolled, four k-steps per trip, after a peeled first
-// trip.
-template <int K_IN, int NB>
+// ahead, four k-steps per trip.
+// `side(h)`, h = 0 .. K_IN/32 - 1, is independent vector work (the previous
+// block's epilogue) issued between the products of k-steps 2h and 2h+1 so
+// that it runs while the matrix core is busy; with side work the k loop is
+// unrolled, otherwise it is rolled after a peeled first trip.
+template <int K_IN, int NB, bool UNROLL = false, class Side = NoSide>
 __device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const uint8_t *act, int row_bytes,
                                           int nt0, int lane, uint32_t ring, const uint8_t *ring_ptr,
-                                          const f32x16 &init, f32x16 (&acc)[NB])
+                                          const f32x16 &init, f32x16 (&acc)[NB], Side side = Side())
 {
     constexpr int KS = K_IN / 16;
     static_assert(KS % 4 == 0, "k loop");
     const int r0 = (lane & 31) + 32 * nt0;
     const uint8_t *brow = act + r0 * row_bytes;
-    const int sw = lane & 7, half = lane >> 5;
+    const int sw = lane & 15, half = lane >> 5;
     const bf16x8 *wp = Wm + lane;
-    auto load = [&](int slot, int ks, bf16x8 &a, bf16x8 (&b)[NB]) {
-        a = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
-        const int chunk = (((2 * ks + half) ^ sw) & 7) | ((2 * ks + half) & ~7);
+    auto step = [&](int slot, int ks, bool first) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
+        const int chunk = (((2 * ks + half) ^ sw) & 15) | ((2 * ks + half) & ~15);
+        bf16x8 b[NB];
 #pragma unroll
         for (int nt = 0; nt < NB; ++nt)
             b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
-    };
-    auto step = [&](int slot, int ks) {
-        bf16x8 a, b[NB];
-        load(slot, ks, a, b);
 #pragma unroll
-        for (int nt = 0; nt < NB; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], acc[nt], 0, 0, 0);
+        for (int nt = 0; nt < NB; ++nt)
+            acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], first ? init : acc[nt], 0, 0, 0);
     };
-    // refill after k-steps ks, ks+1 of a trip (slots 0, 1) or ks+2, ks+3 (slots 2, 3)
+    // refill slots first_slot, first_slot + 1 with k-steps ks_next, ks_next + 1
     auto refill = [&](int first_slot, int ks_next) {
         if (ks_next < KS) {
             reads_done();
@@ -263,28 +273,26 @@ __device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const u
             fragments_landed<0>();
         }
     };
+    auto trip = [&](int ks) {
+        step(0, ks, ks == 0);
+        side(ks / 2);
+        step(1, ks + 1, false);
+        refill(0, ks + 4);
+        step(2, ks + 2, false);
+        side(ks / 2 + 1);
+        step(3, ks + 3, false);
+        refill(2, ks + 6);
+    };
 #pragma unroll
     for (int q = 0; q < 4; ++q) dma_fragment(wp + q * 64, ring + q * 1024);
     fragments_landed<2>();
-    {   // first trip: the first product adds the bias
-        bf16x8 a, b[NB];
-        load(0, 0, a, b);
+    if constexpr (UNROLL) {
 #pragma unroll
-        for (int nt = 0; nt < NB; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], init, 0, 0, 0);
-        step(1, 1);
-        refill(0, 4);
-        step(2, 2);
-        step(3, 3);
-        refill(2, 6);
-    }
+        for (int ks = 0; ks < KS; ks += 4) trip(ks);
+    } else {
+        trip(0);
 #pragma unroll 1
-    for (int ks = 4; ks < KS; ks += 4) {
-        step(0, ks);
-        step(1, ks + 1);
-        refill(0, ks + 4);
-        step(2, ks + 2);
-        step(3, ks + 3);
-        refill(2, ks + 6);
+        for (int ks = 4; ks < KS; ks += 4) trip(ks);
     }
 }
 
@@ -322,27 +330,40 @@ __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const f
                                           const uint8_t *ring_ptr)
 {
     constexpr int KS = K_IN / 16;
+    constexpr int H = K_IN / 32;                  // side slots of a block
     uint2 staged[2][4][4];
+    f32x16 acc0[4], acc1[4];
+    mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr,
+                       bias_tile(bias, 64 * wave, lane), acc0);
+    // second M-tile; the first one's 16 epilogue groups ride along
+    mma_block<K_IN, 4, true>(Wf + (int64_t)(2 * wave + 1) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr,
+                             bias_tile(bias, 64 * wave + 32, lane), acc1, [&](int h) {
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-        f32x16 acc[4];
-        mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave + mt) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr,
-                           bias_tile(bias, 64 * wave + 32 * mt, lane), acc);
+                                 for (int q = h * 16 / H; q < (h + 1) * 16 / H; ++q)
+                                     staged[0][q & 3][q >> 2] = gelu_group(acc0[q & 3], q >> 2);
+                             });
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+    for (int g = 0; g < 4; ++g)
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) staged[mt][nt][g] = gelu_group(acc[nt], g);
-    }
+        for (int nt = 0; nt < 4; ++nt) staged[1][nt][g] = gelu_group(acc1[nt], g);
     __syncthreads();
+    // Lanes l and l + 32 hold the two halves of each 16-byte chunk; one
+    // cross-half swap per register gives lane l (l < 32) chunk g = 2p and
+    // lane l + 32 chunk g = 2p + 1 of the same row, stored with one 16-byte
+    // write each.
+    const int half = lane >> 5;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
+            for (int p = 0; p < 2; ++p) {
+                const uint2 x = staged[mt][nt][2 * p], y = staged[mt][nt][2 * p + 1];
+                const auto sx = __builtin_amdgcn_permlane32_swap(x.x, y.x, false, false);
+                const auto sy = __builtin_amdgcn_permlane32_swap(x.y, y.y, false, false);
                 const int row = 32 * nt + (lane & 31);
-                const int u = 64 * wave + 32 * mt + 8 * g + 4 * (lane >> 5);
-                *reinterpret_cast<uint2 *>(act + act_offset(row, 1024, u)) = staged[mt][nt][g];
+                const int u = 64 * wave + 32 * mt + 8 * (2 * p + half);
+                *reinterpret_cast<uint4 *>(act + act_offset(row, 1024, u)) = make_uint4(sx[0], sy[0], sx[1], sy[1]);
             }
     __syncthreads();
 }
@@ -382,26 +403,28 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
     // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two N-tiles),
     // GELU, bf16, then the 256 -> 1 dot product
     float part[4] = {0.f, 0.f, 0.f, 0.f};
+    const f32x16 b3 = bias_tile(m.b3, 32 * wave, lane);
+    // epilogue group q of a block of two N-tiles: GELU, bf16, dot with W4
+    auto epilogue = [&](const f32x16 (&acc)[2], int blk, int q) {
+        const int nt = q & 1, g = q >> 1;
+        const uint2 w = *reinterpret_cast<const uint2 *>(m.W4 + 32 * wave + 8 * g + 4 * (lane >> 5));
+        const uint2 y = gelu_group(acc[nt], g);
+        float p = part[2 * blk + nt];
+        p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
+        p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
+        p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
+        p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
+        part[2 * blk + nt] = p;
+    };
+    {
+        f32x16 accA[2], accB[2];
+        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 0, lane, ring, ring_ptr, b3, accA);
+        mma_block<512, 2, true>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2, lane, ring, ring_ptr, b3, accB,
+                                [&](int h) {
+                                    if (h % 2 == 0) epilogue(accA, 0, h / 2);
+                                });
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        f32x16 acc[2];
-        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2 * blk, lane, ring, ring_ptr,
-                          bias_tile(m.b3, 32 * wave, lane), acc);
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int u = 32 * wave + 8 * g + 4 * (lane >> 5);
-            const uint2 w = *reinterpret_cast<const uint2 *>(m.W4 + u);
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                const uint2 y = gelu_group(acc[nt], g);
-                float p = part[2 * blk + nt];
-                p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
-                p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
-                p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
-                p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
-                part[2 * blk + nt] = p;
-            }
-        }
+        for (int q = 0; q < 8; ++q) epilogue(accB, 1, q);
     }
     // per-row partial sums: lanes l and l + 32 hold the same row; the wave's
     // slot of the (now idle) fragment ring collects them
