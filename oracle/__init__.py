@@ -210,3 +210,106 @@ def bf16_round(x: float) -> float:
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+class _Linear(C.Structure):
+    _fields_ = [("n_features", C.c_int32), ("bias", C.c_float), ("mean", C.c_void_p), ("inv_std", C.c_void_p),
+                ("w", C.c_void_p), ("w_onehot", C.c_void_p)]
+
+
+def linear(m: dict, X: np.ndarray):
+    """Ridge scorer: (fp32 scores, binary64 sum of term magnitudes) per row."""
+    X = _c(X, np.float32)
+    keep = [_c(m[n], np.float32) for n in ("mean", "inv_std", "w", "w_onehot")]
+    s = _Linear(int(m["n_features"]), float(m["bias"]), *[a.ctypes.data for a in keep])
+    n = X.shape[0]
+    out = np.empty(n, np.float32)
+    mag = np.empty(n, np.float64)
+    rc = lib().oracle_linear(C.byref(s), _p(X), C.c_int64(X.shape[1]), C.c_int64(n), _p(out), _p(mag))
+    if rc:
+        raise ValueError(f"oracle_linear: status {rc}")
+    return out, mag
+
+
+EVAL_FIELDS = ("mean_regret", "median_regret", "p95_regret", "max_regret", "top1", "top5", "within5",
+               "random_regret", "n_groups")
+
+
+def evaluate(runtimes: np.ndarray, seg: np.ndarray, idx: np.ndarray):
+    """Aggregate selection metrics; returns (dict of EVAL_FIELDS, per-group
+    regret float64, rank int32, ybar float64)."""
+    rt = _c(runtimes, np.float32)
+    seg = _c(seg, np.int64)
+    idx = _c(idx, np.int32)
+    P, k = idx.shape
+    out = np.empty(9, np.float64)
+    reg = np.empty(P, np.float64)
+    rank = np.empty(P, np.int32)
+    ybar = np.empty(P, np.float64)
+    rc = lib().oracle_evaluate(_p(rt), _p(seg), C.c_int64(P), _p(idx), C.c_int32(k), _p(out), _p(reg), _p(rank),
+                               _p(ybar))
+    if rc:
+        raise MemoryError("oracle_evaluate")
+    return dict(zip(EVAL_FIELDS, out.tolist())), reg, rank, ybar
+
+
+def static_config(runtimes: np.ndarray, seg: np.ndarray, config_id: np.ndarray, n_configs: int):
+    """(best id or -1, its group count, its mean y)."""
+    rt = _c(runtimes, np.float32)
+    seg = _c(seg, np.int64)
+    cfg = _c(config_id, np.int32)
+    best, cnt, my = C.c_int32(0), C.c_int32(0), C.c_double(0.0)
+    rc = lib().oracle_static_config(_p(rt), _p(seg), C.c_int64(len(seg) - 1), _p(cfg), C.c_int32(n_configs),
+                                    C.byref(best), C.byref(cnt), C.byref(my))
+    if rc:
+        raise MemoryError("oracle_static_config")
+    return int(best.value), int(cnt.value), float(my.value)
+
+
+def catalogue_size() -> int:
+    lib().oracle_catalogue_size.restype = C.c_int64
+    return int(lib().oracle_catalogue_size())
+
+
+def catalogue_decode(indices, dtype: int) -> dict:
+    """Knob fields of catalogue points (candidate SoA with the library's
+    field widths)."""
+    indices = np.asarray(indices, np.int64)
+    f = np.empty(13, np.int32)
+    rows = np.empty((len(indices), 13), np.int32)
+    for i, v in enumerate(indices):
+        lib().oracle_catalogue_decode(C.c_int64(int(v)), C.c_int(int(dtype)), _p(f))
+        rows[i] = f
+    out = {}
+    for j, n in enumerate(_CAND):
+        out[n] = rows[:, j].astype(np.uint16 if n in ("tile_m", "tile_n", "tile_k", "inst_n") else np.uint8)
+    return out
+
+
+def catalogue_mask(hw: dict, problems: np.ndarray, flags: int = 0):
+    """(mask uint8 [P][catalogue size], valid count int64 [P])."""
+    keep = []
+    pr = _Problems()
+    for n, dt in (("M", np.int32), ("N", np.int32), ("K", np.int32), ("layout", np.uint8), ("dtype", np.uint8)):
+        a = _c(problems[n], dt)
+        keep.append(a)
+        setattr(pr, n, a.ctypes.data)
+    P = len(problems)
+    n = catalogue_size()
+    mask = np.empty((P, n), np.uint8)
+    cnt = np.empty(P, np.int64)
+    h = hw_struct(hw)
+    lib().oracle_catalogue_mask(C.byref(h), C.byref(pr), C.c_int64(P), C.c_int(flags), _p(mask), _p(cnt))
+    return mask, cnt
+
+
+def catalogue_compact(mask: np.ndarray):
+    """Group-contiguous list of valid points: (seg_offsets int64 [P+1],
+    catalogue index int32 [total]) in problem order, ascending index."""
+    seg = np.zeros(mask.shape[0] + 1, np.int64)
+    parts = []
+    for p in range(mask.shape[0]):
+        nz = np.nonzero(mask[p])[0]
+        parts.append(nz.astype(np.int32))
+        seg[p + 1] = seg[p] + len(nz)
+    return seg, (np.concatenate(parts) if parts else np.zeros(0, np.int32))

@@ -89,7 +89,7 @@ CONFIGS = {
 
 MLP_WIDTHS = (128, 512, 512, 256, 1)
 
-_STREAMS = ("problems", "candidates", "noise", "forest", "mlp", "sample")
+_STREAMS = ("problems", "candidates", "noise", "forest", "mlp", "sample", "linear")
 
 
 def _streams(seed: int) -> dict:
@@ -218,8 +218,10 @@ def _empty_cands(R: int) -> dict:
     return {f: np.zeros(R, dt) for f, dt in CAND_FIELDS}
 
 
-def candidates(cfg: Config, probs: np.ndarray):
-    """Return (seg_offsets int64 [P+1], candidate SoA dict of length R)."""
+def candidates(cfg: Config, probs: np.ndarray, with_ids: bool = False):
+    """Return (seg_offsets int64 [P+1], candidate SoA dict of length R), and
+    with ``with_ids`` also the grid index int32 [R] each row was drawn from
+    (its configuration identity across problems)."""
     rng = _streams(cfg.seed)["candidates"]
     P, C = cfg.n_problems, cfg.per_problem
     R = P * C
@@ -274,6 +276,10 @@ def candidates(cfg: Config, probs: np.ndarray):
         c["swizzle"][:] = 1
     c["inst_m_div16"][:] = 4           # 64-row instruction tile
     c["inst_k"][:] = inst_k_row        # 32 bytes of K per instruction
+    if with_ids:
+        if cfg.name == "full":
+            pick = np.tile(np.arange(C), P)
+        return seg, c, pick.astype(np.int32)
     return seg, c
 
 
@@ -379,6 +385,22 @@ def mlp(cfg: Config, cuts: dict | None = None) -> dict:
     return out
 
 
+def linear(cfg: Config, cuts: dict | None = None) -> dict:
+    """Random ridge-style linear scorer over cfg.n_features columns: weights
+    N(0, 1/F), one-hot weights N(0, 0.1^2), bias U(-1, 1); standardisation
+    from the stored column statistics (as for the MLP)."""
+    if cuts is None:
+        cuts = load_cuts(cfg.name)
+    rng = _streams(cfg.seed)["linear"]
+    F = cfg.n_features
+    return {"n_features": F,
+            "bias": float(np.float32(rng.uniform(-1.0, 1.0))),
+            "mean": cuts["mean"][:F].astype(np.float32),
+            "inv_std": cuts["inv_std"][:F].astype(np.float32),
+            "w": rng.normal(0.0, 1.0 / np.sqrt(F), F).astype(np.float32),
+            "w_onehot": rng.normal(0.0, 0.1, 12).astype(np.float32)}
+
+
 def sample_rows(cfg: Config, n: int) -> np.ndarray:
     """Sorted distinct row indices, a seeded uniform sample (all rows if n >= R)."""
     R = cfg.rows
@@ -404,8 +426,9 @@ class Workload:
 def workload(name: str, with_runtimes: bool = True, with_model: bool = True) -> Workload:
     cfg = CONFIGS[name]
     probs = problems(cfg)
-    seg, cands = candidates(cfg, probs)
+    seg, cands, ids = candidates(cfg, probs, with_ids=True)
     w = Workload(cfg, hardware(), probs, seg, cands)
+    w.extra["config_id"] = ids
     if with_runtimes:
         w.runtimes = runtimes(cfg, probs, seg, cands)
     if with_model:
