@@ -251,6 +251,163 @@ int hwsel_regret(const float *runtimes, const int64_t *seg_offsets, int32_t P, c
                  int32_t k, float *regret_top1, float *regret_bestk, int32_t *best_idx,
                  void *stream);
 
+/*
+ * Linear ridge scorer (section "Linear Ridge Baseline", eq. ridge-loss):
+ *   f(x) = bias + sum over numeric columns j of w[j] * z_j
+ *              + sum over categorical columns of w_onehot[slot of its level],
+ *   z_j  = (clean(x_j) - mean[j]) * inv_std[j]   (fp32, two operations; clean
+ *                                                 maps NaN and +-inf to 0).
+ * The categorical columns are the layout and schedule fields, one-hot
+ * encoded with frozen level sets: column 64 (layout, levels 0..3, slots
+ * 0..3), 73 (mainloop schedule, 0..2, slots 4..6), 74 (epilogue schedule,
+ * 0..2, slots 7..9), 75 (tile scheduler, 0..1, slots 10..11); they exist for
+ * n_features 96 and 128.  A value that is not one of its column's levels
+ * encodes to all zeros (adds nothing).  The terms are accumulated in fp32 in a
+ * fixed order.  Device arrays: mean, inv_std, w fp32 [n_features] (w of a
+ * categorical column is not read), w_onehot fp32 [HWSEL_ONEHOT_SLOTS].  The
+ * struct itself is read on the host.
+ */
+#define HWSEL_ONEHOT_SLOTS 12
+typedef struct hwsel_linear {
+    int32_t n_features;            /* 64, 96 or 128 */
+    float bias;
+    const float *mean, *inv_std, *w, *w_onehot;
+} hwsel_linear_t;
+
+/*
+ * scores[r] = f(X[r]) for r < R.  X: fp32 [R][ld], ld >= n_features,
+ * ld % 4 == 0, 16-byte aligned (as written by hwsel_features).
+ * Returns HWSEL_EINVAL for null pointers, R < 1, a bad ld or alignment;
+ * HWSEL_EUNSUPPORTED for another n_features.
+ */
+int hwsel_linear_score(const hwsel_linear_t *lin, const float *X, int64_t R, int64_t ld, float *scores,
+                       void *stream);
+
+/*
+ * The analytic sampling score of section "Candidate Sampling" as a model-free
+ * scorer: scores[r] = n_c / (W S_SM c_M c_N) * S * sqrt(T_M T_N T_K) with n_c
+ * clusters, S_SM = max(1, floor(n_sm / (c_M c_N))) cluster slots and
+ * W = ceil(n_c / S_SM) cluster waves; the same binary64 sequence, and so the
+ * same fp32 value, as feature column 58 of hwsel_features, without writing
+ * the feature matrix.  Arguments and status codes as for hwsel_features
+ * (scores fp32 [R] replaces X, n_features and ld).
+ */
+int hwsel_sample_score(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                       const hwsel_cands_t *cands, int64_t R, float *scores, void *stream);
+
+/*
+ * Selection metrics over problems (section "Selection Regret (The Target
+ * Metric)") and the uniform-random baseline (section "Final Fit and Test
+ * Protocol").  With y(p,c) = t_best / t_c (1 when t_c == t_best, 0 for a NaN
+ * runtime, read as never finishing, unless every runtime is NaN), for each
+ * problem p whose segment is non-empty and whose pick c_hat = idx[p][0] is a
+ * valid local index ("counted" problems):
+ *   regret[p] = 1 - y(p, c_hat)                       binary64
+ *   rank[p]   = 1 + #{c : t_c < t(c_hat)}             minimum-rank ties, NaN
+ *                                                      slowest; 0 if not counted
+ *   ybar[p]   = mean_c y(p, c)                         binary64, NaN if empty
+ * and over counted problems, in problem order, binary64:
+ *   out[0] mean regret, out[1] median, out[2] 95th percentile, out[3] max,
+ *   out[4] Top1 = share with rank 1, out[5] Top5 = share with rank <= 5,
+ *   out[6] Within5% = share with regret <= 0.05, out[7] mean of 1 - ybar
+ *   (expected regret of a uniform pick), out[8] number of counted problems.
+ * Percentiles interpolate linearly between order statistics at position
+ * q (n - 1).  With no counted problem out[0..7] are NaN and out[8] is 0.
+ * ybar and out[7] are sums whose order differs from a sequential sum; every
+ * other output is exact.
+ *   runtimes fp32 [R]; seg_offsets [P+1] as for hwsel_features; idx int32
+ *   [P][k] as from hwsel_topk_per_problem; out fp64 [HWSEL_EVAL_FIELDS];
+ *   regret, rank, ybar [P] (each nullable); workspace of
+ *   hwsel_evaluate_workspace_bytes(P) bytes (device, 256-byte aligned).
+ * Returns HWSEL_EINVAL for null pointers, P < 1, k outside [1, 64], a short
+ * or misaligned workspace.
+ */
+#define HWSEL_EVAL_FIELDS 9
+int hwsel_evaluate_workspace_bytes(int32_t P, size_t *bytes);
+int hwsel_evaluate(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx, int32_t k,
+                   double *out, double *regret, int32_t *rank, double *ybar, void *workspace,
+                   size_t workspace_bytes, void *stream);
+
+/*
+ * Best static configuration (baseline of section "Final Fit and Test
+ * Protocol"): among configuration ids that appear in at least 80% of the P
+ * problems (5 * count >= 4 * P), the one with the highest mean y over the
+ * problems it appears in (y as for hwsel_evaluate; summed in problem order,
+ * binary64); ties go to the lower id.  Within a problem only the first row
+ * (lowest local index) of an id counts; ids outside [0, n_configs) are
+ * ignored.  Results (device): best[0] = id or -1 if none qualifies, best[1] =
+ * its problem count, mean_y[0] = its mean y (NaN if none); its mean regret is
+ * 1 - mean_y.
+ *   config_id int32 [R]: the identity of each row's configuration (e.g. its
+ *   catalogue index); workspace of hwsel_static_config_workspace_bytes(P,
+ *   n_configs) bytes (device, 256-byte aligned).
+ * Returns HWSEL_EINVAL for null pointers, P < 1, n_configs < 1, a short or
+ * misaligned workspace.
+ */
+int hwsel_static_config_workspace_bytes(int32_t P, int32_t n_configs, size_t *bytes);
+int hwsel_static_config(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *config_id,
+                        int32_t n_configs, int32_t *best, double *mean_y, void *workspace, size_t workspace_bytes,
+                        void *stream);
+
+/*
+ * Configuration catalogue (section "Configuration Space", Table
+ * "Configuration knobs"): the HWSEL_CATALOGUE_SIZE = 534,600 points of
+ * tile_m {64,128,192,256} x tile_n {16,32,48,64,80,96,128,192,256} x tile_k
+ * {32,64,128,256,512} x stages {2..12} x cluster (C_M, C_N) in {1,2,4,8,16}^2
+ * with C_M C_N <= 16 (15 pairs, C_M slower) x mainloop {WS, Pingpong,
+ * Cooperative} x epilogue {NoSmem, TMA, TMA-Cooperative} x scheduler
+ * {Persistent, Stream-K} per layout.  Point i is the mixed-radix number of
+ * the value positions, first knob slowest.  Fixed fields: swizzle 1,
+ * instruction tile 64 x T_N x (32 bytes / input element size).
+ *
+ * hwsel_catalogue_mask: mask[p][i] = 1 iff point i is valid for problem p
+ * (Table "Static validity constraints": Stream-K needs the cooperative
+ * mainloop; cooperative needs T_M % 128 == 0; S (T_M + T_N) T_K b + S_epi +
+ * smem_reserved <= smem_per_block_max, with the epilogue storage S_epi of
+ * feature column 26; A column-major needs T_K <= 256 C_N; B row-major needs
+ * T_K <= 256 C_M; with flags bit 0 also the shape guard T_N <= 2M and
+ * T_N <= 2N of section "Validity Constraints"), the same predicates as
+ * feature columns 86 and 87.  n_valid[p] = number of valid points.
+ *   mask uint8 [P][HWSEL_CATALOGUE_SIZE], 4-byte aligned; n_valid int64 [P].
+ * Returns HWSEL_EINVAL for null pointers, P < 1, a misaligned mask or a bad
+ * hardware field.
+ */
+#define HWSEL_CATALOGUE_SIZE 534600
+int hwsel_catalogue_mask(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, uint32_t flags, uint8_t *mask,
+                         int64_t *n_valid, void *stream);
+
+/*
+ * Group-contiguous list of the valid points: seg_offsets[0] = 0,
+ * seg_offsets[p+1] = seg_offsets[p] + n_valid[p], and point[seg_offsets[p] +
+ * j] = the j-th valid point of problem p in ascending order.  Points whose
+ * position is >= capacity are not written (seg_offsets[P] tells the caller
+ * the size needed).
+ *   mask, n_valid as written by hwsel_catalogue_mask; seg_offsets int64 [P+1];
+ *   point int32 [capacity].
+ * Returns HWSEL_EINVAL for null pointers, P < 1, capacity < 0, a misaligned
+ * mask.
+ */
+int hwsel_catalogue_compact(const uint8_t *mask, const int64_t *n_valid, int32_t P, int64_t *seg_offsets,
+                            int32_t *point, int64_t capacity, void *stream);
+
+/*
+ * Candidate rows of catalogue points, ready for hwsel_features: row r of
+ * problem p (segment as for hwsel_features) gets the knobs of point
+ * point[r], or of point r - seg_offsets[p] when point is NULL (the whole
+ * catalogue per problem); inst_k follows the problem's input dtype.  Point
+ * values outside [0, HWSEL_CATALOGUE_SIZE) are clamped into it.
+ *   out: host struct of DEVICE arrays of length R (the field widths of
+ *   hwsel_cands_t).
+ * Returns HWSEL_EINVAL for null pointers, P < 1, R < 1.
+ */
+typedef struct hwsel_cands_out {
+    uint16_t *tile_m, *tile_n, *tile_k, *inst_n;
+    uint8_t *stages, *cluster_m, *cluster_n, *swizzle, *inst_m_div16, *inst_k;
+    uint8_t *kernel_sched, *epi_sched, *tile_sched;
+} hwsel_cands_out_t;
+int hwsel_catalogue_candidates(const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                               const int32_t *point, int64_t R, const hwsel_cands_out_t *out, void *stream);
+
 /* Static text for a status code. */
 const char *hwsel_status_string(int status);
 /* Detail of the last failed call on this thread ("" if none). */

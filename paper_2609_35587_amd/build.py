@@ -1,8 +1,9 @@
 """Build libhwsel.so (the HIP kernels and the C ABI) for gfx950, in-tree.
 
 Every translation unit is compiled with hipcc for gfx950 only; packed-fp32
-instructions are disabled; the feature unit is also compiled without
-multiply-add contraction (its binary64 sequences are part of its contract).
+instructions are disabled; the feature and evaluation units are also compiled
+without multiply-add contraction (their binary64 sequences are part of their
+contract).
 """
 from __future__ import annotations
 
@@ -16,11 +17,12 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhwsel.so")
 ARCH = "gfx950"
-SOURCES = ["api.hip", "features.hip", "forest.hip", "mlp.hip", "select.hip"]
+SOURCES = ["api.hip", "catalogue.hip", "evaluate.hip", "features.hip", "forest.hip", "mlp.hip", "scorers.hip",
+           "select.hip"]
 COMMON = ["-O3", "-std=c++20", "-fPIC", f"--offload-arch={ARCH}", "-fno-fast-math",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-function", "-Wno-unknown-pragmas"]
-PER_FILE = {"features.hip": ["-ffp-contract=off"]}
+PER_FILE = {"features.hip": ["-ffp-contract=off"], "evaluate.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:

@@ -47,22 +47,8 @@ const char *hwsel_status_string(int status)
 
 const char *hwsel_last_error(void) { return g_err; }
 
-int hwsel_features(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
-                   const hwsel_cands_t *cands, int64_t R, int32_t n_features, float *X, int64_t ld,
-                   void *stream)
+static int check_hw(const hwsel_hw_t &hw, const char *fn, hwsel::HwDev *h)
 {
-    static const char *fn = "hwsel_features";
-    if (!problems || !seg_offsets || !cands || !X) return fail(HWSEL_EINVAL, fn, "null pointer");
-    const void *fields[] = {cands->tile_m, cands->tile_n, cands->tile_k, cands->inst_n, cands->stages,
-                            cands->cluster_m, cands->cluster_n, cands->swizzle, cands->inst_m_div16,
-                            cands->inst_k, cands->kernel_sched, cands->epi_sched, cands->tile_sched};
-    for (const void *f : fields)
-        if (!f) return fail(HWSEL_EINVAL, fn, "null candidate field");
-    if (P < 1 || R < 1) return fail(HWSEL_EINVAL, fn, "P=%d R=%lld must be >= 1", P, (long long)R);
-    if (n_features != 64 && n_features != 96 && n_features != 128)
-        return fail(HWSEL_EUNSUPPORTED, fn, "n_features=%d (supported: 64, 96, 128)", n_features);
-    if (ld < n_features || ld % 4 != 0) return fail(HWSEL_EINVAL, fn, "ld=%lld", (long long)ld);
-    if (!aligned16(X)) return fail(HWSEL_EINVAL, fn, "X not 16-byte aligned");
     const int64_t positive[] = {hw.n_sm, hw.smem_per_sm, hw.smem_per_block_max, hw.regs_per_sm,
                                 hw.max_regs_per_thread, hw.max_blocks_per_sm, hw.max_threads_per_sm,
                                 hw.arch_id, hw.llc_bytes, hw.hbm_bw_gbps, hw.peak_gflops[0],
@@ -70,14 +56,162 @@ int hwsel_features(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, co
     for (int64_t v : positive)
         if (v < 1) return fail(HWSEL_EINVAL, fn, "hardware field %lld < 1", (long long)v);
     if (hw.smem_reserved < 0) return fail(HWSEL_EINVAL, fn, "smem_reserved < 0");
-    const hwsel::HwDev h{hw.n_sm, hw.smem_per_sm, hw.smem_per_block_max, hw.smem_reserved, hw.regs_per_sm,
-                         hw.max_regs_per_thread, hw.max_blocks_per_sm, hw.max_threads_per_sm, hw.arch_id,
-                         hw.llc_bytes, hw.hbm_bw_gbps, {hw.peak_gflops[0], hw.peak_gflops[1], hw.peak_gflops[2]}};
-    const hwsel::CandsDev c{cands->tile_m, cands->tile_n, cands->tile_k, cands->inst_n, cands->stages,
+    *h = hwsel::HwDev{hw.n_sm, hw.smem_per_sm, hw.smem_per_block_max, hw.smem_reserved, hw.regs_per_sm,
+                      hw.max_regs_per_thread, hw.max_blocks_per_sm, hw.max_threads_per_sm, hw.arch_id,
+                      hw.llc_bytes, hw.hbm_bw_gbps, {hw.peak_gflops[0], hw.peak_gflops[1], hw.peak_gflops[2]}};
+    return HWSEL_OK;
+}
+
+// Shared checks of the problem/candidate inputs; fills the kernel views.
+static int check_rows(const hwsel_hw_t &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                      const hwsel_cands_t *cands, int64_t R, const char *fn, hwsel::HwDev *h, hwsel::CandsDev *c)
+{
+    if (!problems || !seg_offsets || !cands) return fail(HWSEL_EINVAL, fn, "null pointer");
+    const void *fields[] = {cands->tile_m, cands->tile_n, cands->tile_k, cands->inst_n, cands->stages,
                             cands->cluster_m, cands->cluster_n, cands->swizzle, cands->inst_m_div16,
                             cands->inst_k, cands->kernel_sched, cands->epi_sched, cands->tile_sched};
+    for (const void *f : fields)
+        if (!f) return fail(HWSEL_EINVAL, fn, "null candidate field");
+    if (P < 1 || R < 1) return fail(HWSEL_EINVAL, fn, "P=%d R=%lld must be >= 1", P, (long long)R);
+    if (int st = check_hw(hw, fn, h)) return st;
+    *c = hwsel::CandsDev{cands->tile_m, cands->tile_n, cands->tile_k, cands->inst_n, cands->stages,
+                         cands->cluster_m, cands->cluster_n, cands->swizzle, cands->inst_m_div16,
+                         cands->inst_k, cands->kernel_sched, cands->epi_sched, cands->tile_sched};
+    return HWSEL_OK;
+}
+
+int hwsel_features(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                   const hwsel_cands_t *cands, int64_t R, int32_t n_features, float *X, int64_t ld,
+                   void *stream)
+{
+    static const char *fn = "hwsel_features";
+    hwsel::HwDev h;
+    hwsel::CandsDev c;
+    if (int st = check_rows(hw, problems, P, seg_offsets, cands, R, fn, &h, &c)) return st;
+    if (!X) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (n_features != 64 && n_features != 96 && n_features != 128)
+        return fail(HWSEL_EUNSUPPORTED, fn, "n_features=%d (supported: 64, 96, 128)", n_features);
+    if (ld < n_features || ld % 4 != 0) return fail(HWSEL_EINVAL, fn, "ld=%lld", (long long)ld);
+    if (!aligned16(X)) return fail(HWSEL_EINVAL, fn, "X not 16-byte aligned");
     return launched(hwsel::launch_features(h, problems, P, seg_offsets, c, R, n_features, X, ld,
                                            (hipStream_t)stream),
+                    fn);
+}
+
+int hwsel_sample_score(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                       const hwsel_cands_t *cands, int64_t R, float *scores, void *stream)
+{
+    static const char *fn = "hwsel_sample_score";
+    hwsel::HwDev h;
+    hwsel::CandsDev c;
+    if (int st = check_rows(hw, problems, P, seg_offsets, cands, R, fn, &h, &c)) return st;
+    if (!scores) return fail(HWSEL_EINVAL, fn, "null pointer");
+    return launched(hwsel::launch_sample_score(h, problems, P, seg_offsets, c, R, scores, (hipStream_t)stream), fn);
+}
+
+int hwsel_linear_score(const hwsel_linear_t *lin, const float *X, int64_t R, int64_t ld, float *scores,
+                       void *stream)
+{
+    static const char *fn = "hwsel_linear_score";
+    if (!lin || !X || !scores || !lin->mean || !lin->inv_std || !lin->w || !lin->w_onehot)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (lin->n_features != 64 && lin->n_features != 96 && lin->n_features != 128)
+        return fail(HWSEL_EUNSUPPORTED, fn, "n_features=%d (supported: 64, 96, 128)", lin->n_features);
+    if (R < 1) return fail(HWSEL_EINVAL, fn, "R=%lld", (long long)R);
+    if (ld < lin->n_features || ld % 4 != 0) return fail(HWSEL_EINVAL, fn, "ld=%lld", (long long)ld);
+    if (!aligned16(X)) return fail(HWSEL_EINVAL, fn, "X not 16-byte aligned");
+    return launched(hwsel::launch_linear(*lin, X, R, ld, scores, (hipStream_t)stream), fn);
+}
+
+int hwsel_evaluate_workspace_bytes(int32_t P, size_t *bytes)
+{
+    static const char *fn = "hwsel_evaluate_workspace_bytes";
+    if (!bytes) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1) return fail(HWSEL_EINVAL, fn, "P=%d", P);
+    *bytes = hwsel::evaluate_workspace_bytes(P);
+    g_err[0] = 0;
+    return HWSEL_OK;
+}
+
+int hwsel_evaluate(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx, int32_t k,
+                   double *out, double *regret, int32_t *rank, double *ybar, void *workspace,
+                   size_t workspace_bytes, void *stream)
+{
+    static const char *fn = "hwsel_evaluate";
+    if (!runtimes || !seg_offsets || !idx || !out || !workspace) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1) return fail(HWSEL_EINVAL, fn, "P=%d", P);
+    if (k < 1 || k > 64) return fail(HWSEL_EINVAL, fn, "k=%d (1..64)", k);
+    const size_t need = hwsel::evaluate_workspace_bytes(P);
+    if (workspace_bytes < need) return fail(HWSEL_EINVAL, fn, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(HWSEL_EINVAL, fn, "workspace not 256-byte aligned");
+    return launched(hwsel::launch_evaluate(runtimes, seg_offsets, P, idx, k, out, regret, rank, ybar, workspace,
+                                           (hipStream_t)stream),
+                    fn);
+}
+
+int hwsel_static_config_workspace_bytes(int32_t P, int32_t n_configs, size_t *bytes)
+{
+    static const char *fn = "hwsel_static_config_workspace_bytes";
+    if (!bytes) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1 || n_configs < 1) return fail(HWSEL_EINVAL, fn, "P=%d n_configs=%d", P, n_configs);
+    *bytes = hwsel::static_config_workspace_bytes(P, n_configs);
+    g_err[0] = 0;
+    return HWSEL_OK;
+}
+
+int hwsel_static_config(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *config_id,
+                        int32_t n_configs, int32_t *best, double *mean_y, void *workspace, size_t workspace_bytes,
+                        void *stream)
+{
+    static const char *fn = "hwsel_static_config";
+    if (!runtimes || !seg_offsets || !config_id || !best || !mean_y || !workspace)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1 || n_configs < 1) return fail(HWSEL_EINVAL, fn, "P=%d n_configs=%d", P, n_configs);
+    const size_t need = hwsel::static_config_workspace_bytes(P, n_configs);
+    if (workspace_bytes < need) return fail(HWSEL_EINVAL, fn, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(HWSEL_EINVAL, fn, "workspace not 256-byte aligned");
+    return launched(hwsel::launch_static_config(runtimes, seg_offsets, P, config_id, n_configs, best, mean_y,
+                                                workspace, (hipStream_t)stream),
+                    fn);
+}
+
+int hwsel_catalogue_mask(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, uint32_t flags, uint8_t *mask,
+                         int64_t *n_valid, void *stream)
+{
+    static const char *fn = "hwsel_catalogue_mask";
+    hwsel::HwDev h;
+    if (!problems || !mask || !n_valid) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1) return fail(HWSEL_EINVAL, fn, "P=%d", P);
+    if (((uintptr_t)mask & 3u) != 0) return fail(HWSEL_EINVAL, fn, "mask not 4-byte aligned");
+    if (int st = check_hw(hw, fn, &h)) return st;
+    return launched(hwsel::launch_catalogue_mask(h, problems, P, flags, mask, n_valid, (hipStream_t)stream), fn);
+}
+
+int hwsel_catalogue_compact(const uint8_t *mask, const int64_t *n_valid, int32_t P, int64_t *seg_offsets,
+                            int32_t *point, int64_t capacity, void *stream)
+{
+    static const char *fn = "hwsel_catalogue_compact";
+    if (!mask || !n_valid || !seg_offsets || (!point && capacity > 0)) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1 || capacity < 0) return fail(HWSEL_EINVAL, fn, "P=%d capacity=%lld", P, (long long)capacity);
+    if (((uintptr_t)mask & 3u) != 0) return fail(HWSEL_EINVAL, fn, "mask not 4-byte aligned");
+    return launched(hwsel::launch_catalogue_compact(mask, n_valid, P, seg_offsets, point, capacity,
+                                                    (hipStream_t)stream),
+                    fn);
+}
+
+int hwsel_catalogue_candidates(const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                               const int32_t *point, int64_t R, const hwsel_cands_out_t *out, void *stream)
+{
+    static const char *fn = "hwsel_catalogue_candidates";
+    if (!problems || !seg_offsets || !out) return fail(HWSEL_EINVAL, fn, "null pointer");
+    const void *fields[] = {out->tile_m, out->tile_n, out->tile_k, out->inst_n, out->stages, out->cluster_m,
+                            out->cluster_n, out->swizzle, out->inst_m_div16, out->inst_k, out->kernel_sched,
+                            out->epi_sched, out->tile_sched};
+    for (const void *f : fields)
+        if (!f) return fail(HWSEL_EINVAL, fn, "null candidate field");
+    if (P < 1 || R < 1) return fail(HWSEL_EINVAL, fn, "P=%d R=%lld", P, (long long)R);
+    return launched(hwsel::launch_catalogue_candidates(problems, P, seg_offsets, point, R, *out,
+                                                       (hipStream_t)stream),
                     fn);
 }
 

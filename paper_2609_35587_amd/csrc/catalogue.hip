@@ -1,0 +1,203 @@
+// Configuration catalogue (section "Configuration Space", Table
+// "Configuration knobs") and its static validity mask (section "Validity
+// Constraints", Table "Static validity constraints").
+//
+// A point index decodes to its knobs by mixed radix (first knob slowest), so
+// the mask pass never stores the catalogue: each thread decodes four
+// consecutive points and writes their four mask bytes as one word.  The
+// compaction is one workgroup per problem, an ordered block-wide scan over
+// the problem's mask.
+#include "internal.hpp"
+
+namespace hwsel {
+namespace {
+
+constexpr int64_t kCat = HWSEL_CATALOGUE_SIZE;
+__constant__ int16_t kTileM[4] = {64, 128, 192, 256};
+__constant__ int16_t kTileN[9] = {16, 32, 48, 64, 80, 96, 128, 192, 256};
+__constant__ int16_t kTileK[5] = {32, 64, 128, 256, 512};
+// (C_M, C_N) in {1,2,4,8,16}^2 with C_M C_N <= 16, C_M slower
+__constant__ uint8_t kClusterM[15] = {1, 1, 1, 1, 1, 2, 2, 2, 2, 4, 4, 4, 8, 8, 16};
+__constant__ uint8_t kClusterN[15] = {1, 2, 4, 8, 16, 1, 2, 4, 8, 1, 2, 4, 1, 2, 1};
+
+struct Knobs {
+    int32_t tm, tn, tk, st, cm, cn, ks, es, ts;
+};
+
+__device__ __forceinline__ Knobs decode(int64_t i)
+{
+    Knobs k;
+    k.ts = (int32_t)(i % 2); i /= 2;
+    k.es = (int32_t)(i % 3); i /= 3;
+    k.ks = (int32_t)(i % 3); i /= 3;
+    const int32_t cl = (int32_t)(i % 15); i /= 15;
+    k.st = 2 + (int32_t)(i % 11); i /= 11;
+    k.tk = kTileK[i % 5]; i /= 5;
+    k.tn = kTileN[i % 9]; i /= 9;
+    k.tm = kTileM[i];
+    k.cm = kClusterM[cl];
+    k.cn = kClusterN[cl];
+    return k;
+}
+
+__device__ __forceinline__ bool valid(const HwDev &h, const hwsel_problem_t &pb, uint32_t flags, const Knobs &k)
+{
+    const int64_t M = pb.M > 1 ? pb.M : 1, N = pb.N > 1 ? pb.N : 1;
+    const int layout = pb.layout < 3 ? pb.layout : 3;
+    const int64_t b = (pb.dtype < 2 ? pb.dtype : 2) == 2 ? 1 : 2;
+    const int64_t frag = (int64_t)(k.tm < 64 ? k.tm : 64) * (k.tn < 32 ? k.tn : 32) * 2;
+    const int64_t epi = k.es == 0 ? 0 : (k.es == 1 ? 2 * frag : 4 * frag);
+    bool ok = k.ts != 1 || k.ks == 2;                                   // Stream-K needs cooperative
+    ok &= k.ks != 2 || k.tm % 128 == 0;                                 // cooperative splits T_M in two
+    ok &= (int64_t)k.st * (k.tm + k.tn) * k.tk * b + epi + h.smem_rsv <= h.smem_block;
+    if (layout == 2 || layout == 3) ok &= k.tk <= 256 * k.cn;           // A column-major
+    if (layout == 1 || layout == 3) ok &= k.tk <= 256 * k.cm;           // B row-major
+    if (flags & 1u) ok &= k.tn <= 2 * M && k.tn <= 2 * N;
+    return ok;
+}
+
+__global__ void k_zero_i64(int64_t *__restrict__ a, int32_t n)
+{
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) a[i] = 0;
+}
+
+constexpr int kMaskThreads = 256;
+constexpr int64_t kWords = (kCat + 3) / 4;
+
+__global__ __launch_bounds__(kMaskThreads) void k_catalogue_mask(HwDev h, const hwsel_problem_t *__restrict__ probs,
+                                                                 int32_t P, uint32_t flags, uint8_t *__restrict__ mask,
+                                                                 int64_t *__restrict__ n_valid)
+{
+    __shared__ int32_t red[kMaskThreads];
+    for (int32_t p = blockIdx.y; p < P; p += gridDim.y) {
+    const hwsel_problem_t pb = probs[p];
+    const int64_t w = (int64_t)blockIdx.x * kMaskThreads + threadIdx.x;
+    int32_t cnt = 0;
+    if (w < kWords) {
+        uint32_t word = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t i = 4 * w + q;
+            if (i < kCat && valid(h, pb, flags, decode(i))) {
+                word |= 1u << (8 * q);
+                ++cnt;
+            }
+        }
+        uint8_t *row = mask + (int64_t)p * kCat;
+        // kCat is a multiple of 4 and every row starts 4-byte aligned when mask is
+        *reinterpret_cast<uint32_t *>(row + 4 * w) = word;
+    }
+    red[threadIdx.x] = cnt;
+    __syncthreads();
+    for (int s = kMaskThreads / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0 && red[0]) atomicAdd(reinterpret_cast<unsigned long long *>(n_valid + p),
+                                              (unsigned long long)red[0]);
+    __syncthreads();
+    }
+}
+
+__global__ void k_catalogue_offsets(const int64_t *__restrict__ n_valid, int32_t P, int64_t *__restrict__ seg)
+{
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        int64_t acc = 0;
+        seg[0] = 0;
+        for (int32_t p = 0; p < P; ++p) {
+            acc += n_valid[p] > 0 ? n_valid[p] : 0;
+            seg[p + 1] = acc;
+        }
+    }
+}
+
+constexpr int kCompactThreads = 1024;
+
+__global__ __launch_bounds__(kCompactThreads) void k_catalogue_compact(const uint8_t *__restrict__ mask,
+                                                                       const int64_t *__restrict__ seg,
+                                                                       int32_t *__restrict__ point, int64_t cap)
+{
+    __shared__ int32_t scan[kCompactThreads];
+    const int32_t p = blockIdx.x;
+    const uint32_t *row = reinterpret_cast<const uint32_t *>(mask + (int64_t)p * kCat);
+    int64_t out = seg[p];
+    for (int64_t w0 = 0; w0 < kWords; w0 += kCompactThreads) {
+        const int64_t w = w0 + threadIdx.x;
+        const uint32_t word = w < kWords ? row[w] : 0u;
+        const int32_t c = (int32_t)((word & 1u) + ((word >> 8) & 1u) + ((word >> 16) & 1u) + ((word >> 24) & 1u));
+        scan[threadIdx.x] = c;
+        __syncthreads();
+        // inclusive Hillis-Steele scan
+        for (int s = 1; s < kCompactThreads; s <<= 1) {
+            const int32_t v = threadIdx.x >= s ? scan[threadIdx.x - s] : 0;
+            __syncthreads();
+            scan[threadIdx.x] += v;
+            __syncthreads();
+        }
+        int64_t pos = out + scan[threadIdx.x] - c;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if ((word >> (8 * q)) & 1u) {
+                if (pos < cap) point[pos] = (int32_t)(4 * w + q);
+                ++pos;
+            }
+        out += scan[kCompactThreads - 1];
+        __syncthreads();
+    }
+}
+
+__global__ void k_catalogue_candidates(const hwsel_problem_t *__restrict__ probs, int32_t P,
+                                       const int64_t *__restrict__ seg, const int32_t *__restrict__ point, int64_t R,
+                                       hwsel_cands_out_t out)
+{
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= R) return;
+    const int32_t p = segment_of_row(seg, P, r);
+    int64_t i = point ? (int64_t)point[r] : r - seg[p];
+    i = i < 0 ? 0 : (i >= kCat ? kCat - 1 : i);
+    const Knobs k = decode(i);
+    const int dt = probs[p].dtype < 2 ? probs[p].dtype : 2;
+    out.tile_m[r] = (uint16_t)k.tm;
+    out.tile_n[r] = (uint16_t)k.tn;
+    out.tile_k[r] = (uint16_t)k.tk;
+    out.inst_n[r] = (uint16_t)k.tn;
+    out.stages[r] = (uint8_t)k.st;
+    out.cluster_m[r] = (uint8_t)k.cm;
+    out.cluster_n[r] = (uint8_t)k.cn;
+    out.swizzle[r] = 1;
+    out.inst_m_div16[r] = 4;
+    out.inst_k[r] = dt == 2 ? 32 : 16;
+    out.kernel_sched[r] = (uint8_t)k.ks;
+    out.epi_sched[r] = (uint8_t)k.es;
+    out.tile_sched[r] = (uint8_t)k.ts;
+}
+
+}  // namespace
+
+hipError_t launch_catalogue_mask(const HwDev &h, const hwsel_problem_t *probs, int32_t P, uint32_t flags,
+                                 uint8_t *mask, int64_t *n_valid, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_zero_i64, dim3((P + 255) / 256), dim3(256), 0, s, n_valid, P);
+    const dim3 grid((unsigned)((kWords + kMaskThreads - 1) / kMaskThreads), (unsigned)(P < 65535 ? P : 65535));
+    hipLaunchKernelGGL(k_catalogue_mask, grid, dim3(kMaskThreads), 0, s, h, probs, P, flags, mask, n_valid);
+    return hipGetLastError();
+}
+
+hipError_t launch_catalogue_compact(const uint8_t *mask, const int64_t *n_valid, int32_t P, int64_t *seg,
+                                    int32_t *point, int64_t cap, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_catalogue_offsets, dim3(1), dim3(64), 0, s, n_valid, P, seg);
+    hipLaunchKernelGGL(k_catalogue_compact, dim3(P), dim3(kCompactThreads), 0, s, mask, seg, point, cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_catalogue_candidates(const hwsel_problem_t *probs, int32_t P, const int64_t *seg,
+                                       const int32_t *point, int64_t R, const hwsel_cands_out_t &out, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_catalogue_candidates, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, probs, P, seg,
+                       point, R, out);
+    return hipGetLastError();
+}
+
+}  // namespace hwsel

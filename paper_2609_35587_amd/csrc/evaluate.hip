@@ -1,0 +1,321 @@
+// Selection metrics and baselines over problems (section "Selection Regret
+// (The Target Metric)"; baselines of section "Final Fit and Test Protocol").
+//
+// Per-problem passes read each segment once (one workgroup per problem);
+// the aggregates are exact order statistics and fixed-order binary64 sums
+// over at most a few hundred thousand problems.
+#include <limits.h>
+
+#include "internal.hpp"
+
+namespace hwsel {
+namespace {
+
+constexpr int kEvalThreads = 256;
+
+// Strictly faster runtime; NaN is slower than everything, +inf included.
+__device__ __forceinline__ bool faster(float a, float b)
+{
+    const bool na = a != a, nb = b != b;
+    if (na || nb) return !na && nb;
+    return a < b;
+}
+
+// y = t_best / t: 1 for equal runtimes (inf included), 0 for NaN.
+__device__ __forceinline__ double y_of(float t_best, float t)
+{
+    if (t == t_best) return 1.0;
+    if (t != t) return 0.0;
+    return (double)t_best / (double)t;
+}
+
+// Fastest runtime of rows [base, base + n) for a whole workgroup.
+__device__ float block_fastest(const float *__restrict__ rt, int64_t base, int64_t n, float *red)
+{
+    float best = __builtin_nanf("");
+    for (int64_t j = threadIdx.x; j < n; j += blockDim.x) {
+        const float t = rt[base + j];
+        if (faster(t, best)) best = t;
+    }
+    red[threadIdx.x] = best;
+    __syncthreads();
+    for (int s = blockDim.x / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s && faster(red[threadIdx.x + s], red[threadIdx.x])) red[threadIdx.x] = red[threadIdx.x + s];
+        __syncthreads();
+    }
+    const float out = red[0];
+    __syncthreads();
+    return out;
+}
+
+// Fixed-shape tree sums over the workgroup (same order every run).
+__device__ double block_sum(double v, double *red)
+{
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = blockDim.x / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    const double out = red[0];
+    __syncthreads();
+    return out;
+}
+
+__device__ int64_t block_count(int64_t v, int64_t *red)
+{
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = blockDim.x / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    const int64_t out = red[0];
+    __syncthreads();
+    return out;
+}
+
+__global__ __launch_bounds__(kEvalThreads) void k_eval_groups(const float *__restrict__ rt,
+                                                              const int64_t *__restrict__ seg, int32_t P,
+                                                              const int32_t *__restrict__ idx, int32_t k,
+                                                              double *__restrict__ regret, int32_t *__restrict__ rank,
+                                                              double *__restrict__ ybar)
+{
+    __shared__ double red[kEvalThreads];
+    const int32_t p = blockIdx.x;
+    const int64_t base = seg[p], n = seg[p + 1] - seg[p];
+    if (n <= 0) {
+        if (threadIdx.x == 0) {
+            regret[p] = __builtin_nan("");
+            rank[p] = 0;
+            ybar[p] = __builtin_nan("");
+        }
+        return;
+    }
+    const float t_best = block_fastest(rt, base, n, reinterpret_cast<float *>(red));
+    const int32_t sel = idx[(int64_t)p * k];
+    const bool counted = sel >= 0 && sel < n;
+    const float t_sel = counted ? rt[base + sel] : 0.0f;
+    double ys = 0.0;
+    int64_t nb = 0;
+    for (int64_t j = threadIdx.x; j < n; j += kEvalThreads) {
+        const float t = rt[base + j];
+        ys += y_of(t_best, t);
+        nb += faster(t, t_sel) ? 1 : 0;
+    }
+    ys = block_sum(ys, red);
+    nb = block_count(nb, reinterpret_cast<int64_t *>(red));
+    if (threadIdx.x == 0) {
+        ybar[p] = ys / (double)n;
+        regret[p] = counted ? 1.0 - y_of(t_best, t_sel) : __builtin_nan("");
+        rank[p] = counted ? (int32_t)(1 + nb) : 0;
+    }
+}
+
+// sorted[position of problem i among counted regrets] = regret[i]; the
+// position counts smaller values and equal values of lower index.
+__global__ __launch_bounds__(kEvalThreads) void k_eval_order(const double *__restrict__ regret,
+                                                             const int32_t *__restrict__ rank, int32_t P,
+                                                             double *__restrict__ sorted)
+{
+    const int32_t i = blockIdx.x * kEvalThreads + threadIdx.x;
+    if (i >= P || rank[i] == 0) return;
+    const double v = regret[i];
+    int64_t pos = 0;
+    for (int32_t j = 0; j < P; ++j) {
+        if (rank[j] == 0) continue;
+        const double u = regret[j];
+        pos += (u < v || (u == v && j < i)) ? 1 : 0;
+    }
+    sorted[pos] = v;
+}
+
+__device__ double percentile(const double *s, int64_t n, double q)
+{
+    const double pos = q * (double)(n - 1);
+    const int64_t lo = (int64_t)__builtin_floor(pos);
+    const int64_t hi = lo + 1 < n ? lo + 1 : n - 1;
+    return s[lo] + (pos - (double)lo) * (s[hi] - s[lo]);
+}
+
+__global__ void k_eval_aggregate(const double *__restrict__ regret, const int32_t *__restrict__ rank,
+                                 const double *__restrict__ ybar, const double *__restrict__ sorted, int32_t P,
+                                 double *__restrict__ out, double *__restrict__ regret_out,
+                                 int32_t *__restrict__ rank_out, double *__restrict__ ybar_out)
+{
+    if (threadIdx.x == 0) {
+        int64_t cnt = 0, top1 = 0, top5 = 0, w5 = 0;
+        double sum = 0.0, rsum = 0.0, mx = -__builtin_inf();
+        for (int32_t p = 0; p < P; ++p) {
+            if (rank[p] == 0) continue;
+            const double r = regret[p];
+            ++cnt;
+            sum += r;
+            rsum += 1.0 - ybar[p];
+            mx = r > mx ? r : mx;
+            top1 += rank[p] == 1;
+            top5 += rank[p] <= 5;
+            w5 += r <= 0.05;
+        }
+        if (cnt == 0) {
+            for (int i = 0; i < 8; ++i) out[i] = __builtin_nan("");
+            out[8] = 0.0;
+        } else {
+            out[0] = sum / (double)cnt;
+            out[1] = percentile(sorted, cnt, 0.5);
+            out[2] = percentile(sorted, cnt, 0.95);
+            out[3] = mx;
+            out[4] = (double)top1 / (double)cnt;
+            out[5] = (double)top5 / (double)cnt;
+            out[6] = (double)w5 / (double)cnt;
+            out[7] = rsum / (double)cnt;
+            out[8] = (double)cnt;
+        }
+    }
+    for (int32_t p = threadIdx.x; p < P; p += blockDim.x) {
+        if (regret_out) regret_out[p] = regret[p];
+        if (rank_out) rank_out[p] = rank[p];
+        if (ybar_out) ybar_out[p] = ybar[p];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Best static configuration
+// ---------------------------------------------------------------------------
+__global__ void k_fill_i32(int32_t *__restrict__ a, int64_t n, int32_t v)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        a[i] = v;
+}
+
+// first[p][id] = lowest local index of id in problem p's segment.
+__global__ void k_static_first(const int64_t *__restrict__ seg, int32_t P, const int32_t *__restrict__ cfg,
+                               int32_t n_cfg, int32_t *__restrict__ first)
+{
+    const int64_t R = seg[P];
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < R; r += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t id = cfg[r];
+        if (id < 0 || id >= n_cfg) continue;
+        const int32_t p = segment_of_row(seg, P, r);
+        if (r < seg[p] || r >= seg[p + 1]) continue;
+        atomicMin(&first[(int64_t)p * n_cfg + id], (int32_t)(r - seg[p]));
+    }
+}
+
+__global__ __launch_bounds__(kEvalThreads) void k_static_best_time(const float *__restrict__ rt,
+                                                                   const int64_t *__restrict__ seg,
+                                                                   float *__restrict__ t_best)
+{
+    __shared__ float red[kEvalThreads];
+    const int32_t p = blockIdx.x;
+    const int64_t n = seg[p + 1] - seg[p];
+    const float t = block_fastest(rt, seg[p], n > 0 ? n : 0, red);
+    if (threadIdx.x == 0) t_best[p] = t;
+}
+
+__global__ void k_static_accumulate(const float *__restrict__ rt, const int64_t *__restrict__ seg, int32_t P,
+                                    int32_t n_cfg, const int32_t *__restrict__ first,
+                                    const float *__restrict__ t_best, int32_t *__restrict__ count,
+                                    double *__restrict__ ysum)
+{
+    const int32_t id = blockIdx.x * blockDim.x + threadIdx.x;
+    if (id >= n_cfg) return;
+    int32_t c = 0;
+    double s = 0.0;
+    for (int32_t p = 0; p < P; ++p) {
+        const int32_t j = first[(int64_t)p * n_cfg + id];
+        if (j == INT_MAX) continue;
+        ++c;
+        s += y_of(t_best[p], rt[seg[p] + j]);
+    }
+    count[id] = c;
+    ysum[id] = s;
+}
+
+__global__ __launch_bounds__(1024) void k_static_argmax(const int32_t *__restrict__ count,
+                                                        const double *__restrict__ ysum, int32_t n_cfg, int32_t P,
+                                                        int32_t *__restrict__ best, double *__restrict__ mean_y)
+{
+    __shared__ double red_y[1024];
+    __shared__ int32_t red_id[1024];
+    int32_t bid = -1;
+    double by = 0.0;
+    for (int32_t id = threadIdx.x; id < n_cfg; id += 1024) {
+        const int64_t c = count[id];
+        if (c == 0 || 5 * c < 4 * (int64_t)P) continue;
+        const double m = ysum[id] / (double)c;
+        if (bid < 0 || m > by) { bid = id; by = m; }   // ids ascend within a thread
+    }
+    red_y[threadIdx.x] = by;
+    red_id[threadIdx.x] = bid;
+    __syncthreads();
+    for (int s = 512; s > 0; s >>= 1) {
+        if (threadIdx.x < s) {
+            const int32_t o = red_id[threadIdx.x + s], m = red_id[threadIdx.x];
+            const double oy = red_y[threadIdx.x + s], my = red_y[threadIdx.x];
+            if (o >= 0 && (m < 0 || oy > my || (oy == my && o < m))) {
+                red_id[threadIdx.x] = o;
+                red_y[threadIdx.x] = oy;
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const int32_t b = red_id[0];
+        best[0] = b;
+        best[1] = b < 0 ? 0 : count[b];
+        mean_y[0] = b < 0 ? __builtin_nan("") : red_y[0];
+    }
+}
+
+size_t up256(size_t v) { return (v + 255) / 256 * 256; }
+
+}  // namespace
+
+size_t evaluate_workspace_bytes(int32_t P)
+{
+    return 3 * up256((size_t)P * sizeof(double)) + up256((size_t)P * sizeof(int32_t));
+}
+
+hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx, int32_t k,
+                           double *out, double *regret_out, int32_t *rank_out, double *ybar_out, void *ws,
+                           hipStream_t s)
+{
+    uint8_t *w = static_cast<uint8_t *>(ws);
+    double *regret = reinterpret_cast<double *>(w);
+    double *ybar = reinterpret_cast<double *>(w + up256((size_t)P * 8));
+    double *sorted = reinterpret_cast<double *>(w + 2 * up256((size_t)P * 8));
+    int32_t *rank = reinterpret_cast<int32_t *>(w + 3 * up256((size_t)P * 8));
+    hipLaunchKernelGGL(k_eval_groups, dim3(P), dim3(kEvalThreads), 0, s, rt, seg, P, idx, k, regret, rank, ybar);
+    hipLaunchKernelGGL(k_eval_order, dim3((P + kEvalThreads - 1) / kEvalThreads), dim3(kEvalThreads), 0, s, regret,
+                       rank, P, sorted);
+    hipLaunchKernelGGL(k_eval_aggregate, dim3(1), dim3(256), 0, s, regret, rank, ybar, sorted, P, out, regret_out,
+                       rank_out, ybar_out);
+    return hipGetLastError();
+}
+
+size_t static_config_workspace_bytes(int32_t P, int32_t n_cfg)
+{
+    return up256((size_t)P * (size_t)n_cfg * sizeof(int32_t)) + up256((size_t)P * sizeof(float)) +
+           up256((size_t)n_cfg * sizeof(int32_t)) + up256((size_t)n_cfg * sizeof(double));
+}
+
+hipError_t launch_static_config(const float *rt, const int64_t *seg, int32_t P, const int32_t *cfg, int32_t n_cfg,
+                                int32_t *best, double *mean_y, void *ws, hipStream_t s)
+{
+    uint8_t *w = static_cast<uint8_t *>(ws);
+    const size_t table = up256((size_t)P * (size_t)n_cfg * sizeof(int32_t));
+    int32_t *first = reinterpret_cast<int32_t *>(w);
+    float *t_best = reinterpret_cast<float *>(w + table);
+    int32_t *count = reinterpret_cast<int32_t *>(w + table + up256((size_t)P * 4));
+    double *ysum = reinterpret_cast<double *>(w + table + up256((size_t)P * 4) + up256((size_t)n_cfg * 4));
+    hipLaunchKernelGGL(k_fill_i32, dim3(2048), dim3(256), 0, s, first, (int64_t)P * n_cfg, (int32_t)INT_MAX);
+    hipLaunchKernelGGL(k_static_first, dim3(2048), dim3(256), 0, s, seg, P, cfg, n_cfg, first);
+    hipLaunchKernelGGL(k_static_best_time, dim3(P), dim3(kEvalThreads), 0, s, rt, seg, t_best);
+    hipLaunchKernelGGL(k_static_accumulate, dim3((n_cfg + 255) / 256), dim3(256), 0, s, rt, seg, P, n_cfg, first,
+                       t_best, count, ysum);
+    hipLaunchKernelGGL(k_static_argmax, dim3(1), dim3(1024), 0, s, count, ysum, n_cfg, P, best, mean_y);
+    return hipGetLastError();
+}
+
+}  // namespace hwsel

@@ -37,6 +37,15 @@ constexpr int tStreamK = 1;
 constexpr int dFp16 = 1, dFp8 = 2, dFp32 = 3;
 constexpr int lNN = 2, lNT = 3, lTT = 1;
 
+// Analytic sampling score (section "Candidate Sampling"): the cluster-wave
+// fill n_c / (W S_SM c_M c_N) times S sqrt(T_M T_N T_K), in binary64.
+__device__ __forceinline__ float sampling_score(int64_t clusters, int64_t cwaves, int64_t cslots, int64_t cm,
+                                                int64_t cn, int64_t st, int64_t tm, int64_t tn, int64_t tk)
+{
+    const double fill = (double)(clusters * st) / (double)(cwaves * cslots * cm * cn);
+    return (float)(fill * sqrt((double)(tm * tn * tk)));
+}
+
 template <int F>
 __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, const CandsDev &c,
                                     int64_t r, float (&x)[F])
@@ -149,10 +158,7 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
     x[55] = quot(st * smem, h.smem_sm);
     x[56] = exact(tk * st);
     x[57] = exact(st * resident);
-    {
-        const double fill = (double)(clusters * st) / (double)(cwaves * cslots * cm * cn);
-        x[58] = (float)(fill * sqrt((double)(tm * tn * tk)));
-    }
+    x[58] = sampling_score(clusters, cwaves, cslots, cm, cn, st, tm, tn, tk);
     x[59] = exact(h.n_sm); x[60] = exact(h.smem_sm); x[61] = exact(h.regs_sm);
     x[62] = exact(h.llc); x[63] = exact(h.bw);
 
@@ -260,7 +266,33 @@ __global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_p
     }
 }
 
+// Sampling score alone, one row per thread.
+__global__ __launch_bounds__(256) void k_sample_score(HwDev h, const hwsel_problem_t *__restrict__ probs, int32_t P,
+                                                       const int64_t *__restrict__ seg, CandsDev c, int64_t R,
+                                                       float *__restrict__ scores)
+{
+    const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (r >= R) return;
+    const hwsel_problem_t pb = probs[segment_of_row(seg, P, r)];
+    const int64_t M = max64(pb.M, 1), N = max64(pb.N, 1);
+    const int64_t tm = max64(c.tile_m[r], 1), tn = max64(c.tile_n[r], 1), tk = max64(c.tile_k[r], 1);
+    const int64_t st = max64(c.stages[r], 1);
+    const int64_t cm = max64(c.cluster_m[r], 1), cn = max64(c.cluster_n[r], 1);
+    const int64_t clusters = cdiv64(M, cm * tm) * cdiv64(N, cn * tn);
+    const int64_t cslots = max64(h.n_sm / (cm * cn), 1);
+    const int64_t cwaves = cdiv64(clusters, cslots);
+    scores[r] = sampling_score(clusters, cwaves, cslots, cm, cn, st, tm, tn, tk);
+}
+
 }  // namespace
+
+hipError_t launch_sample_score(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
+                               const CandsDev &c, int64_t R, float *scores, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_sample_score, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, hw, problems, P, seg, c,
+                       R, scores);
+    return hipGetLastError();
+}
 
 hipError_t launch_features(const HwDev &hw, const hwsel_problem_t *problems, int32_t P,
                            const int64_t *seg, const CandsDev &c, int64_t R, int32_t F, float *X,

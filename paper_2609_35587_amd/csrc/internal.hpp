@@ -28,6 +28,27 @@ hipError_t launch_features(const HwDev &hw, const hwsel_problem_t *problems, int
                            const int64_t *seg, const CandsDev &c, int64_t R, int32_t F, float *X,
                            int64_t ld, hipStream_t s);
 
+hipError_t launch_sample_score(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
+                               const CandsDev &c, int64_t R, float *scores, hipStream_t s);
+
+hipError_t launch_linear(const hwsel_linear_t &lin, const float *X, int64_t R, int64_t ld, float *scores,
+                         hipStream_t s);
+
+size_t evaluate_workspace_bytes(int32_t P);
+hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx, int32_t k,
+                           double *out, double *regret_out, int32_t *rank_out, double *ybar_out, void *ws,
+                           hipStream_t s);
+size_t static_config_workspace_bytes(int32_t P, int32_t n_cfg);
+hipError_t launch_static_config(const float *rt, const int64_t *seg, int32_t P, const int32_t *cfg, int32_t n_cfg,
+                                int32_t *best, double *mean_y, void *ws, hipStream_t s);
+
+hipError_t launch_catalogue_mask(const HwDev &h, const hwsel_problem_t *probs, int32_t P, uint32_t flags,
+                                 uint8_t *mask, int64_t *n_valid, hipStream_t s);
+hipError_t launch_catalogue_compact(const uint8_t *mask, const int64_t *n_valid, int32_t P, int64_t *seg,
+                                    int32_t *point, int64_t cap, hipStream_t s);
+hipError_t launch_catalogue_candidates(const hwsel_problem_t *probs, int32_t P, const int64_t *seg,
+                                       const int32_t *point, int64_t R, const hwsel_cands_out_t &out, hipStream_t s);
+
 hipError_t launch_forest_score(const hwsel_forest_t &f, const float *X, int64_t R, int64_t ld,
                                float *scores, hipStream_t s);
 

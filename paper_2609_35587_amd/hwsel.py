@@ -55,6 +55,15 @@ class hwsel_mlp_t(C.Structure):
                 ("b3", C.c_void_p), ("b4", C.c_void_p)]
 
 
+class hwsel_cands_out_t(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in CAND_FIELDS]
+
+
+class hwsel_linear_t(C.Structure):
+    _fields_ = [("n_features", C.c_int32), ("bias", C.c_float), ("mean", C.c_void_p), ("inv_std", C.c_void_p),
+                ("w", C.c_void_p), ("w_onehot", C.c_void_p)]
+
+
 _lib = None
 
 
@@ -80,6 +89,16 @@ def lib() -> C.CDLL:
         L.hwsel_mlp_pack.argtypes = [C.POINTER(hwsel_mlp_t), vp, C.c_size_t, vp]
         L.hwsel_topk_per_problem.argtypes = [vp, vp, i32, i32, vp, vp, vp]
         L.hwsel_regret.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp]
+        L.hwsel_linear_score.argtypes = [C.POINTER(hwsel_linear_t), vp, i64, i64, vp, vp]
+        sz = C.c_size_t
+        L.hwsel_evaluate_workspace_bytes.argtypes = [i32, C.POINTER(sz)]
+        L.hwsel_evaluate.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.hwsel_static_config_workspace_bytes.argtypes = [i32, i32, C.POINTER(sz)]
+        L.hwsel_static_config.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, sz, vp]
+        L.hwsel_catalogue_mask.argtypes = [hwsel_hw_t, vp, i32, C.c_uint32, vp, vp, vp]
+        L.hwsel_catalogue_compact.argtypes = [vp, vp, i32, vp, vp, i64, vp]
+        L.hwsel_catalogue_candidates.argtypes = [vp, i32, vp, vp, i64, C.POINTER(hwsel_cands_out_t), vp]
+        L.hwsel_sample_score.argtypes = [hwsel_hw_t, vp, i32, vp, C.POINTER(hwsel_cands_t), i64, vp, vp]
         _lib = L
     return _lib
 
@@ -148,6 +167,36 @@ def hwsel_features(hw: dict, problems: torch.Tensor, seg_offsets: torch.Tensor, 
         hw_struct(hw), _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")),
         C.byref(cs), R, n_features, _ptr(X), X.stride(0), _stream(stream)))
     return X
+
+
+def hwsel_sample_score(hw: dict, problems: torch.Tensor, seg_offsets: torch.Tensor, cands: dict,
+                       scores: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The analytic sampling score per row (no feature matrix)."""
+    P = problems.shape[0]
+    R = cands["tile_m"].shape[0]
+    if scores is None:
+        scores = torch.empty(R, dtype=torch.float32, device=problems.device)
+    cs = hwsel_cands_t(*[_ptr(_dev(cands[n], n)) for n in CAND_FIELDS])
+    _check("hwsel_sample_score", lib().hwsel_sample_score(
+        hw_struct(hw), _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")),
+        C.byref(cs), R, _ptr(scores), _stream(stream)))
+    return scores
+
+
+def linear_struct(m: dict) -> hwsel_linear_t:
+    return hwsel_linear_t(int(m["n_features"]), float(m["bias"]), _ptr(m["mean"]), _ptr(m["inv_std"]),
+                          _ptr(m["w"]), _ptr(m["w_onehot"]))
+
+
+def hwsel_linear_score(lin: dict, X: torch.Tensor, scores: torch.Tensor | None = None,
+                       stream=None) -> torch.Tensor:
+    R = X.shape[0]
+    if scores is None:
+        scores = torch.empty(R, dtype=torch.float32, device=X.device)
+    s = linear_struct(lin)
+    _check("hwsel_linear_score", lib().hwsel_linear_score(C.byref(s), _ptr(X), R, X.stride(0), _ptr(scores),
+                                                          _stream(stream)))
+    return scores
 
 
 def forest_struct(f: dict) -> hwsel_forest_t:
@@ -267,6 +316,92 @@ def hwsel_regret(runtimes: torch.Tensor, seg_offsets: torch.Tensor, idx: torch.T
         _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P, _ptr(_dev(idx, "idx")), k,
         _ptr(r1), _ptr(rk), _ptr(best), _stream(stream)))
     return r1, rk, best
+
+
+HWSEL_EVAL_FIELDS = 9
+HWSEL_CATALOGUE_SIZE = 534600
+
+
+def hwsel_evaluate(runtimes: torch.Tensor, seg_offsets: torch.Tensor, idx: torch.Tensor,
+                   workspace: torch.Tensor | None = None, per_group: bool = True, stream=None):
+    """Returns (out fp64 [9], regret fp64 [P], rank int32 [P], ybar fp64 [P]);
+    the per-group arrays are None unless per_group."""
+    P, k = idx.shape
+    dev = runtimes.device
+    n = C.c_size_t(0)
+    _check("hwsel_evaluate_workspace_bytes", lib().hwsel_evaluate_workspace_bytes(P, C.byref(n)))
+    if workspace is None:
+        workspace = torch.empty(int(n.value), dtype=torch.uint8, device=dev)
+    out = torch.empty(HWSEL_EVAL_FIELDS, dtype=torch.float64, device=dev)
+    reg = rank = ybar = None
+    if per_group:
+        reg = torch.empty(P, dtype=torch.float64, device=dev)
+        rank = torch.empty(P, dtype=torch.int32, device=dev)
+        ybar = torch.empty(P, dtype=torch.float64, device=dev)
+    _check("hwsel_evaluate", lib().hwsel_evaluate(
+        _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P, _ptr(_dev(idx, "idx")), k,
+        _ptr(out), _ptr(reg), _ptr(rank), _ptr(ybar), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out, reg, rank, ybar
+
+
+def hwsel_static_config(runtimes: torch.Tensor, seg_offsets: torch.Tensor, config_id: torch.Tensor,
+                        n_configs: int, workspace: torch.Tensor | None = None, stream=None):
+    """Returns (best int32 [2] = (id, count), mean_y fp64 [1]) on the device."""
+    P = seg_offsets.shape[0] - 1
+    dev = runtimes.device
+    n = C.c_size_t(0)
+    _check("hwsel_static_config_workspace_bytes",
+           lib().hwsel_static_config_workspace_bytes(P, n_configs, C.byref(n)))
+    if workspace is None:
+        workspace = torch.empty(int(n.value), dtype=torch.uint8, device=dev)
+    best = torch.empty(2, dtype=torch.int32, device=dev)
+    mean_y = torch.empty(1, dtype=torch.float64, device=dev)
+    _check("hwsel_static_config", lib().hwsel_static_config(
+        _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P,
+        _ptr(_dev(config_id, "config_id")), n_configs, _ptr(best), _ptr(mean_y), _ptr(workspace),
+        workspace.numel(), _stream(stream)))
+    return best, mean_y
+
+
+def hwsel_catalogue_mask(hw: dict, problems: torch.Tensor, flags: int = 0, mask: torch.Tensor | None = None,
+                         stream=None):
+    """Returns (mask uint8 [P, 534600], n_valid int64 [P])."""
+    P = problems.shape[0]
+    dev = problems.device
+    if mask is None:
+        mask = torch.empty((P, HWSEL_CATALOGUE_SIZE), dtype=torch.uint8, device=dev)
+    n_valid = torch.empty(P, dtype=torch.int64, device=dev)
+    _check("hwsel_catalogue_mask", lib().hwsel_catalogue_mask(
+        hw_struct(hw), _ptr(_dev(problems, "problems")), P, flags, _ptr(mask), _ptr(n_valid), _stream(stream)))
+    return mask, n_valid
+
+
+def hwsel_catalogue_compact(mask: torch.Tensor, n_valid: torch.Tensor, capacity: int,
+                            point: torch.Tensor | None = None, stream=None):
+    """Returns (seg_offsets int64 [P+1], point int32 [capacity])."""
+    P = mask.shape[0]
+    dev = mask.device
+    seg = torch.empty(P + 1, dtype=torch.int64, device=dev)
+    if point is None:
+        point = torch.empty(max(capacity, 1), dtype=torch.int32, device=dev)
+    _check("hwsel_catalogue_compact", lib().hwsel_catalogue_compact(
+        _ptr(_dev(mask, "mask")), _ptr(_dev(n_valid, "n_valid")), P, _ptr(seg), _ptr(point), capacity,
+        _stream(stream)))
+    return seg, point
+
+
+def hwsel_catalogue_candidates(problems: torch.Tensor, seg_offsets: torch.Tensor, R: int,
+                               point: torch.Tensor | None = None, stream=None) -> dict:
+    """Candidate SoA (name -> device tensor of length R) of catalogue points."""
+    P = problems.shape[0]
+    dev = problems.device
+    wide = ("tile_m", "tile_n", "tile_k", "inst_n")
+    out = {n: torch.empty(R, dtype=torch.int16 if n in wide else torch.uint8, device=dev) for n in CAND_FIELDS}
+    s = hwsel_cands_out_t(*[_ptr(out[n]) for n in CAND_FIELDS])
+    _check("hwsel_catalogue_candidates", lib().hwsel_catalogue_candidates(
+        _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")), _ptr(point), R, C.byref(s),
+        _stream(stream)))
+    return out
 
 
 def declared_functions() -> list[str]:

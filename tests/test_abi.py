@@ -126,3 +126,51 @@ def test_forest_packed_rejects(L):
     wide = hwsel.forest_struct(dict(f, n_features=200))
     assert L.hwsel_forest_pack_bytes(C.byref(wide), C.byref(n)) == 2
     assert L.hwsel_forest_score(C.byref(wide), FAKE, FAKE, 1000, 200, FAKE, FAKE, 1 << 30, None) == 2
+
+
+def test_cheap_scorers_reject(L):
+    lin = hwsel.hwsel_linear_t(128, 0.0, FAKE, FAKE, FAKE, FAKE)
+    assert L.hwsel_linear_score(C.byref(lin), FAKE, 0, 128, FAKE, None) == 1
+    assert L.hwsel_linear_score(C.byref(lin), FAKE, 10, 126, FAKE, None) == 1
+    assert L.hwsel_linear_score(C.byref(lin), FAKE + 4, 10, 128, FAKE, None) == 1
+    assert L.hwsel_linear_score(C.byref(lin), FAKE, 10, 128, None, None) == 1
+    assert L.hwsel_linear_score(C.byref(hwsel.hwsel_linear_t(100, 0.0, FAKE, FAKE, FAKE, FAKE)), FAKE, 10, 128,
+                                FAKE, None) == 2
+    assert L.hwsel_linear_score(C.byref(hwsel.hwsel_linear_t(64, 0.0, FAKE, FAKE, FAKE, None)), FAKE, 10, 64,
+                                FAKE, None) == 1
+    assert L.hwsel_sample_score(_hw(), FAKE, 4, FAKE, C.byref(_cands()), 0, FAKE, None) == 1
+    assert L.hwsel_sample_score(_hw(n_sm=0), FAKE, 4, FAKE, C.byref(_cands()), 10, FAKE, None) == 1
+    assert L.hwsel_sample_score(_hw(), FAKE, 4, FAKE, C.byref(_cands(tile_k=1)), 10, FAKE, None) == 1
+    assert L.hwsel_sample_score(_hw(), FAKE, 4, FAKE, C.byref(_cands()), 10, None, None) == 1
+    assert L.hwsel_last_error().startswith(b"hwsel_sample_score: ")
+
+
+def test_evaluation_rejects(L):
+    n = C.c_size_t(0)
+    assert L.hwsel_evaluate_workspace_bytes(600, C.byref(n)) == 0 and n.value >= 600 * 28
+    ws = n.value
+    assert L.hwsel_evaluate(FAKE, FAKE, 0, FAKE, 10, FAKE, None, None, None, FAKE, ws, None) == 1
+    assert L.hwsel_evaluate(FAKE, FAKE, 600, FAKE, 65, FAKE, None, None, None, FAKE, ws, None) == 1
+    assert L.hwsel_evaluate(FAKE, FAKE, 600, FAKE, 10, FAKE, None, None, None, FAKE, ws - 1, None) == 1
+    assert L.hwsel_evaluate(FAKE, FAKE, 600, FAKE, 10, FAKE, None, None, None, FAKE + 16, ws, None) == 1
+    assert L.hwsel_evaluate(FAKE, FAKE, 600, FAKE, 10, None, None, None, None, FAKE, ws, None) == 1
+    assert L.hwsel_static_config_workspace_bytes(600, 0, C.byref(n)) == 1
+    assert L.hwsel_static_config_workspace_bytes(600, 65536, C.byref(n)) == 0
+    assert n.value >= 600 * 65536 * 4
+    assert L.hwsel_static_config(FAKE, FAKE, 600, FAKE, 65536, FAKE, FAKE, FAKE, n.value - 1, None) == 1
+    assert L.hwsel_static_config(FAKE, FAKE, 600, None, 65536, FAKE, FAKE, FAKE, n.value, None) == 1
+    assert L.hwsel_static_config(FAKE, FAKE, 600, FAKE, 65536, FAKE, FAKE, FAKE + 8, n.value, None) == 1
+
+
+def test_catalogue_rejects(L):
+    assert L.hwsel_catalogue_mask(_hw(), FAKE, 0, 0, FAKE, FAKE, None) == 1
+    assert L.hwsel_catalogue_mask(_hw(), FAKE, 4, 0, FAKE + 2, FAKE, None) == 1
+    assert L.hwsel_catalogue_mask(_hw(llc_bytes=0), FAKE, 4, 0, FAKE, FAKE, None) == 1
+    assert L.hwsel_catalogue_mask(_hw(), FAKE, 4, 0, FAKE, None, None) == 1
+    assert L.hwsel_catalogue_compact(FAKE, FAKE, 4, FAKE, FAKE, -1, None) == 1
+    assert L.hwsel_catalogue_compact(FAKE, FAKE, 4, FAKE, None, 10, None) == 1
+    assert L.hwsel_catalogue_compact(FAKE + 1, FAKE, 4, FAKE, FAKE, 10, None) == 1
+    out = hwsel.hwsel_cands_out_t(*([FAKE] * 12 + [None]))
+    assert L.hwsel_catalogue_candidates(FAKE, 4, FAKE, None, 10, C.byref(out), None) == 1
+    out = hwsel.hwsel_cands_out_t(*([FAKE] * 13))
+    assert L.hwsel_catalogue_candidates(FAKE, 4, FAKE, None, 0, C.byref(out), None) == 1

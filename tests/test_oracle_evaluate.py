@@ -114,3 +114,11 @@ def test_static_config_hand_built():
     assert (best2, cnt2) == (7, 5) and my2 == pytest.approx(y7, rel=1e-15)
     best3, _, my3 = oracle.static_config(rt, seg, np.arange(len(cfg), dtype=np.int32), len(cfg))
     assert best3 == -1 and np.isnan(my3)
+
+
+def test_nan_runtime_reads_as_never_finishing():
+    rt = np.array([1.0, np.nan, np.nan, np.nan], np.float32)
+    seg = np.array([0, 2, 4], np.int64)
+    agg, reg, rank, ybar = oracle.evaluate(rt, seg, np.array([[1], [0]], np.int32))
+    assert reg.tolist() == [1.0, 1.0] and rank.tolist() == [2, 1]
+    assert ybar.tolist() == [0.5, 0.0]
