@@ -252,6 +252,28 @@ int hwsel_regret(const float *runtimes, const int64_t *seg_offsets, int32_t P, c
                  void *stream);
 
 /*
+ * Fused selection with a packed forest, the scored path in one call (section
+ * "Problem Formulation": features, scorer, per-problem argmax generalised to
+ * the k best) without materialising the feature matrix: each row's feature
+ * vector phi(p, c, h) (n_features columns) is binned against the forest's
+ * thresholds as it is computed, the bins are scored, and the scores go to
+ * the per-problem top-k.  idx, vals and scores are bit-identical to
+ * hwsel_features -> hwsel_forest_score (with `packed`) ->
+ * hwsel_topk_per_problem on the same inputs.
+ *   Inputs as for hwsel_features and hwsel_forest_score; f->n_features must
+ *   be <= n_features.  idx int32 [P][k], vals fp32 [P][k] (nullable), scores
+ *   fp32 [R] (nullable); workspace of hwsel_select_forest_workspace_bytes(f,
+ *   R) bytes (device, 256-byte aligned).
+ * Returns the status codes of those calls, and HWSEL_EINVAL when
+ * f->n_features > n_features.
+ */
+int hwsel_select_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *bytes);
+int hwsel_select_forest(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                        const hwsel_cands_t *cands, int64_t R, int32_t n_features, const hwsel_forest_t *f,
+                        const void *packed, int32_t k, int32_t *idx, float *vals, float *scores, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/*
  * Linear ridge scorer (section "Linear Ridge Baseline", eq. ridge-loss):
  *   f(x) = bias + sum over numeric columns j of w[j] * z_j
  *              + sum over categorical columns of w_onehot[slot of its level],

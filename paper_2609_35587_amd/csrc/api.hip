@@ -296,6 +296,52 @@ int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int6
     return launched(hwsel::launch_forest_leaves(*f, X, R, ld, rows, n_rows, leaf_idx, (hipStream_t)stream), fn);
 }
 
+int hwsel_select_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *bytes)
+{
+    static const char *fn = "hwsel_select_forest_workspace_bytes";
+    size_t dummy = 0;
+    if (int s = hwsel_forest_pack_bytes(f, &dummy)) return s;
+    if (!bytes) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (R < 1) return fail(HWSEL_EINVAL, fn, "R=%lld", (long long)R);
+    *bytes = hwsel::packed_workspace_bytes(*f, R) + ((size_t)R * sizeof(float) + 255) / 256 * 256;
+    return HWSEL_OK;
+}
+
+int hwsel_select_forest(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg_offsets,
+                        const hwsel_cands_t *cands, int64_t R, int32_t n_features, const hwsel_forest_t *f,
+                        const void *packed, int32_t k, int32_t *idx, float *vals, float *scores, void *workspace,
+                        size_t workspace_bytes, void *stream)
+{
+    static const char *fn = "hwsel_select_forest";
+    hwsel::HwDev h;
+    hwsel::CandsDev c;
+    if (int st = check_rows(hw, problems, P, seg_offsets, cands, R, fn, &h, &c)) return st;
+    if (n_features != 64 && n_features != 96 && n_features != 128)
+        return fail(HWSEL_EUNSUPPORTED, fn, "n_features=%d (supported: 64, 96, 128)", n_features);
+    if (!f || !packed || !idx || !workspace || !f->node_feature || !f->node_threshold || !f->leaf_value)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (f->n_trees < 1) return fail(HWSEL_EINVAL, fn, "n_trees=%d", f->n_trees);
+    if (!hwsel::packable(*f)) return fail(HWSEL_EUNSUPPORTED, fn, "forest shape cannot be packed");
+    if (f->n_features < 1 || f->n_features > n_features)
+        return fail(HWSEL_EINVAL, fn, "forest n_features=%d, feature map has %d", f->n_features, n_features);
+    if (k < 1 || k > 64) return fail(HWSEL_EINVAL, fn, "k=%d (1..64)", k);
+    if (!aligned16(packed)) return fail(HWSEL_EINVAL, fn, "packed not 16-byte aligned");
+    const size_t base = hwsel::packed_workspace_bytes(*f, R);
+    const size_t need = base + ((size_t)R * sizeof(float) + 255) / 256 * 256;
+    if (workspace_bytes < need)
+        return fail(HWSEL_EINVAL, fn, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(HWSEL_EINVAL, fn, "workspace not 256-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    float *sc = scores ? scores : reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + base);
+    hipError_t e = hwsel::launch_features_bins(h, problems, P, seg_offsets, c, R, n_features,
+                                               hwsel::packed_thresholds(packed), f->n_features,
+                                               hwsel::packed_nan_bin(*f), static_cast<uint8_t *>(workspace),
+                                               hwsel::packed_bin_stride(*f), s);
+    if (e == hipSuccess) e = hwsel::launch_forest_from_bins(*f, packed, R, sc, workspace, s);
+    if (e == hipSuccess) e = hwsel::launch_topk(sc, seg_offsets, P, k, idx, vals, s);
+    return launched(e, fn);
+}
+
 static int check_mlp(const hwsel_mlp_t *m, const char *fn)
 {
     if (!m || !m->mean || !m->inv_std || !m->W1 || !m->W2 || !m->W3 || !m->W4 || !m->b1 || !m->b2 || !m->b3 ||

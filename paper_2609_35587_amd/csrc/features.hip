@@ -284,7 +284,76 @@ __global__ __launch_bounds__(256) void k_sample_score(HwDev h, const hwsel_probl
     scores[r] = sampling_score(clusters, cwaves, cslots, cm, cn, st, tm, tn, tk);
 }
 
+// Features straight to forest bins: the row's feature vector stays in
+// registers and each of the first nf columns is binned against the forest's
+// sorted thresholds (b = #{u : u <= x}, NaN to nan_bin), the same search as
+// the forest's own binning pass; X is never written.  One workgroup per CU
+// holds the threshold table in LDS and walks row tiles.
+constexpr int kFbThreads = 256;
+constexpr int kFbSlots = 256;
+constexpr int kFbStride = 257;
+
+template <int F>
+__global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const hwsel_problem_t *__restrict__ probs,
+                                                                 int32_t P, const int64_t *__restrict__ seg,
+                                                                 CandsDev c, int64_t R, const float *__restrict__ U,
+                                                                 int nf, uint32_t nan_bin, uint8_t *__restrict__ Xb,
+                                                                 int stride)
+{
+    __shared__ float u[128 * kFbStride];
+    for (int e = threadIdx.x; e < nf * kFbSlots; e += kFbThreads) u[(e >> 8) * kFbStride + (e & 255)] = U[e];
+    __syncthreads();
+    for (int64_t r = (int64_t)blockIdx.x * kFbThreads + threadIdx.x; r < R; r += (int64_t)gridDim.x * kFbThreads) {
+        float x[F];
+        const int32_t p = segment_of_row(seg, P, r);
+        const hwsel_problem_t pb = probs[p];
+        phi<F>(h, pb, c, r, x);
+        uint32_t word[F / 4];
+#pragma unroll
+        for (int q = 0; q < F / 4; ++q) word[q] = 0;
+#pragma unroll
+        for (int f = 0; f < F; ++f) {
+            if (f < nf) {
+                const float *uf = u + f * kFbStride;
+                uint32_t b = 0;
+#pragma unroll
+                for (int step = 128; step > 0; step >>= 1) b += (uf[b + step - 1] <= x[f]) ? step : 0;
+                if (x[f] != x[f]) b = nan_bin;
+                word[f / 4] |= b << (8 * (f % 4));
+            }
+        }
+        uint8_t *dst = Xb + r * stride;
+#pragma unroll
+        for (int q = 0; q < F / 16; ++q)
+            if (16 * q < stride)
+                *reinterpret_cast<uint4 *>(dst + 16 * q) =
+                    make_uint4(word[4 * q], word[4 * q + 1], word[4 * q + 2], word[4 * q + 3]);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_features_bins(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
+                                const CandsDev &c, int64_t R, int32_t F, const float *U, int nf, uint32_t nan_bin,
+                                uint8_t *Xb, int stride, hipStream_t s)
+{
+    int dev = 0, n_cu = 256;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+        n_cu = 256;
+    const int64_t need = (R + kFbThreads - 1) / kFbThreads;
+    const unsigned blocks = (unsigned)(need < n_cu ? need : n_cu);
+    if (F == 64)
+        hipLaunchKernelGGL(k_features_bins<64>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R, U,
+                           nf, nan_bin, Xb, stride);
+    else if (F == 96)
+        hipLaunchKernelGGL(k_features_bins<96>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R, U,
+                           nf, nan_bin, Xb, stride);
+    else
+        hipLaunchKernelGGL(k_features_bins<128>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R,
+                           U, nf, nan_bin, Xb, stride);
+    return hipGetLastError();
+}
 
 hipError_t launch_sample_score(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
                                const CandsDev &c, int64_t R, float *scores, hipStream_t s)

@@ -455,24 +455,40 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
     return PackStatus::ok;
 }
 
+const float *packed_thresholds(const void *packed)
+{
+    return reinterpret_cast<const float *>(static_cast<const uint8_t *>(packed) + 256);
+}
+
+int packed_bin_stride(const hwsel_forest_t &f) { return geometry(f).stride; }
+
+uint32_t packed_nan_bin(const hwsel_forest_t &f) { return (f.flags & 1u) ? 0u : 255u; }
+
 hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
                                 int64_t ld, float *scores, void *workspace, hipStream_t s)
 {
     const PackGeom g = geometry(f);
-    const uint8_t *base = static_cast<const uint8_t *>(packed);
-    const float *U = reinterpret_cast<const float *>(base + 256);
-    const uint8_t *chunks = base + 256 + g.thr_bytes;
     uint8_t *Xb = static_cast<uint8_t *>(workspace);
-    float *partial = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + align256((size_t)R * g.stride));
-    const uint32_t nan_bin = (f.flags & 1u) ? 0u : 255u;
     int dev = 0, n_cu = 256;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
         n_cu = 256;
-    hipLaunchKernelGGL(k_bin, dim3(n_cu), dim3(kBinThreads), 0, s, X, R, ld, U, f.n_features, nan_bin, Xb, g.stride);
+    hipLaunchKernelGGL(k_bin, dim3(n_cu), dim3(kBinThreads), 0, s, X, R, ld, packed_thresholds(packed),
+                       f.n_features, packed_nan_bin(f), Xb, g.stride);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_traverse(f.depth, chunks, g.n_chunks, Xb, R, g.stride, partial, s);
+    return launch_forest_from_bins(f, packed, R, scores, workspace, s);
+}
+
+// Traversal and reduction of bins already in the workspace.
+hipError_t launch_forest_from_bins(const hwsel_forest_t &f, const void *packed, int64_t R, float *scores,
+                                   void *workspace, hipStream_t s)
+{
+    const PackGeom g = geometry(f);
+    const uint8_t *chunks = static_cast<const uint8_t *>(packed) + 256 + g.thr_bytes;
+    const uint8_t *Xb = static_cast<const uint8_t *>(workspace);
+    float *partial = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + align256((size_t)R * g.stride));
+    hipError_t e = launch_traverse(f.depth, chunks, g.n_chunks, Xb, R, g.stride, partial, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_reduce, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
                        f.base_score, scores);

@@ -64,6 +64,17 @@ size_t packed_workspace_bytes(const hwsel_forest_t &f, int64_t R);
 PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s);
 hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
                                 int64_t ld, float *scores, void *workspace, hipStream_t s);
+// Pieces of the packed path for the fused selection: the threshold table and
+// bin-row geometry of an image, and the traversal of bins already written to
+// the start of the workspace.
+const float *packed_thresholds(const void *packed);
+int packed_bin_stride(const hwsel_forest_t &f);
+uint32_t packed_nan_bin(const hwsel_forest_t &f);
+hipError_t launch_forest_from_bins(const hwsel_forest_t &f, const void *packed, int64_t R, float *scores,
+                                   void *workspace, hipStream_t s);
+hipError_t launch_features_bins(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
+                                const CandsDev &c, int64_t R, int32_t F, const float *U, int nf, uint32_t nan_bin,
+                                uint8_t *Xb, int stride, hipStream_t s);
 
 hipError_t launch_mlp(const hwsel_mlp_t &m, const float *X, int64_t R, int64_t ld, float *scores,
                       hipStream_t s);

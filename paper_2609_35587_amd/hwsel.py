@@ -91,6 +91,9 @@ def lib() -> C.CDLL:
         L.hwsel_regret.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp]
         L.hwsel_linear_score.argtypes = [C.POINTER(hwsel_linear_t), vp, i64, i64, vp, vp]
         sz = C.c_size_t
+        L.hwsel_select_forest_workspace_bytes.argtypes = [C.POINTER(hwsel_forest_t), i64, C.POINTER(sz)]
+        L.hwsel_select_forest.argtypes = [hwsel_hw_t, vp, i32, vp, C.POINTER(hwsel_cands_t), i64, i32,
+                                          C.POINTER(hwsel_forest_t), vp, i32, vp, vp, vp, vp, sz, vp]
         L.hwsel_evaluate_workspace_bytes.argtypes = [i32, C.POINTER(sz)]
         L.hwsel_evaluate.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]
         L.hwsel_static_config_workspace_bytes.argtypes = [i32, i32, C.POINTER(sz)]
@@ -316,6 +319,37 @@ def hwsel_regret(runtimes: torch.Tensor, seg_offsets: torch.Tensor, idx: torch.T
         _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P, _ptr(_dev(idx, "idx")), k,
         _ptr(r1), _ptr(rk), _ptr(best), _stream(stream)))
     return r1, rk, best
+
+
+def hwsel_select_forest_workspace_bytes(forest: dict, R: int) -> int:
+    n = C.c_size_t(0)
+    s = forest_struct(forest)
+    _check("hwsel_select_forest_workspace_bytes", lib().hwsel_select_forest_workspace_bytes(C.byref(s), R,
+                                                                                            C.byref(n)))
+    return int(n.value)
+
+
+def hwsel_select_forest(hw: dict, problems: torch.Tensor, seg_offsets: torch.Tensor, cands: dict, n_features: int,
+                        forest: dict, packed: torch.Tensor, k: int, workspace: torch.Tensor | None = None,
+                        idx: torch.Tensor | None = None, vals: torch.Tensor | None = None,
+                        scores: torch.Tensor | None = None, with_vals: bool = True, stream=None):
+    """Fused features -> packed forest -> top-k; returns (idx, vals, scores)."""
+    P = problems.shape[0]
+    R = cands["tile_m"].shape[0]
+    dev = problems.device
+    if workspace is None:
+        workspace = torch.empty(hwsel_select_forest_workspace_bytes(forest, R), dtype=torch.uint8, device=dev)
+    if idx is None:
+        idx = torch.empty((P, k), dtype=torch.int32, device=dev)
+    if vals is None and with_vals:
+        vals = torch.empty((P, k), dtype=torch.float32, device=dev)
+    cs = hwsel_cands_t(*[_ptr(_dev(cands[n], n)) for n in CAND_FIELDS])
+    f = forest_struct(forest)
+    _check("hwsel_select_forest", lib().hwsel_select_forest(
+        hw_struct(hw), _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")), C.byref(cs), R,
+        n_features, C.byref(f), _ptr(packed), k, _ptr(idx), _ptr(vals), _ptr(scores), _ptr(workspace),
+        workspace.numel(), _stream(stream)))
+    return idx, vals, scores
 
 
 HWSEL_EVAL_FIELDS = 9

@@ -7,6 +7,7 @@ import sys
 import numpy as np
 import torch
 
+import oracle
 from paper_2609_35587_amd import hwsel
 
 INT_COLS_T1 = [4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 20, 22, 23, 24, 25, 26, 27, 29, 30, 31, 32, 33, 36,
@@ -79,3 +80,24 @@ def assert_forest_scores(g: np.ndarray, o: np.ndarray, l1: np.ndarray, tol: floa
     i = int(np.argmax(err - bound))
     assert np.all(err <= bound), f"row {i}: gpu {g[i]} oracle {o[i]} bound {bound[i]}"
     return float((err / np.maximum(bound, 1e-30)).max())
+
+
+def check_selection(w, idx, problems):
+    """The GPU's per-problem choice (idx [P][k], from the GPU's own scores)
+    against the oracle's features -> forest -> top-k on every row of the given
+    problems.  The forest's fp32 leaf sums may order two candidates whose
+    oracle scores lie within the score tolerance differently: such a swap is
+    accepted only when it is explained by that near-tie."""
+    cfg = w.cfg
+    for p in problems:
+        rows = np.arange(w.seg[p], w.seg[p + 1], dtype=np.int64)
+        Xp = oracle.features(w.hw, w.problems, w.seg, w.cands, cfg.n_features, rows)
+        o, oli = oracle.forest(w.forest, Xp, leaves=True)
+        oidx, _ = oracle.topk(o, np.array([0, len(rows)], np.int64), cfg.k)
+        if np.array_equal(idx[p], oidx[0]):
+            continue
+        tol = 2e-5 * np.maximum(np.abs(o.astype(np.float64)), path_l1(w.forest, oli))
+        for a, b in zip(idx[p], oidx[0]):
+            if a != b:
+                assert abs(float(o[a]) - float(o[b])) <= tol[a] + tol[b], f"problem {p}: {a} vs {b}"
+        say(f"  problem {p}: order differs only on near-ties")

@@ -174,3 +174,33 @@ def test_catalogue_rejects(L):
     assert L.hwsel_catalogue_candidates(FAKE, 4, FAKE, None, 10, C.byref(out), None) == 1
     out = hwsel.hwsel_cands_out_t(*([FAKE] * 13))
     assert L.hwsel_catalogue_candidates(FAKE, 4, FAKE, None, 0, C.byref(out), None) == 1
+
+
+def test_fused_selection_rejects(L):
+    f = dict(n_trees=10, depth=8, n_features=96, flags=1, base_score=0.0, node_feature=FAKE,
+             node_threshold=FAKE, leaf_value=FAKE)
+    s = hwsel.forest_struct(f)
+    n = C.c_size_t(0)
+    assert L.hwsel_select_forest_workspace_bytes(C.byref(s), 1000, C.byref(n)) == 0
+    ws = n.value
+    w = C.c_size_t(0)
+    assert L.hwsel_forest_workspace_bytes(C.byref(s), 1000, C.byref(w)) == 0 and ws >= w.value + 4000
+
+    def call(**over):
+        a = dict(hw=_hw(), problems=FAKE, P=4, seg=FAKE, cands=_cands(), R=1000, F=96, f=s, packed=FAKE, k=10,
+                 idx=FAKE, ws=FAKE, wsb=ws)
+        a.update(over)
+        return L.hwsel_select_forest(a["hw"], a["problems"], a["P"], a["seg"], C.byref(a["cands"]), a["R"], a["F"],
+                                     C.byref(a["f"]), a["packed"], a["k"], a["idx"], None, None, a["ws"], a["wsb"],
+                                     None)
+
+    assert call(F=64) == 1                      # forest reads 96 columns, the map has 64
+    assert call(F=100) == 2
+    assert call(k=0) == 1 and call(k=65) == 1
+    assert call(packed=None) == 1 and call(idx=None) == 1
+    assert call(packed=FAKE + 8) == 1
+    assert call(wsb=ws - 1) == 1 and call(ws=FAKE + 16) == 1
+    assert call(P=0) == 1 and call(hw=_hw(n_sm=0)) == 1
+    deep = hwsel.forest_struct(dict(f, depth=11))
+    assert call(f=deep) == 2
+    assert L.hwsel_last_error().startswith(b"hwsel_select_forest: ")

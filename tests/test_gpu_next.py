@@ -238,3 +238,34 @@ def test_catalogue_rows_feed_the_scored_path():
     s = hwsel.hwsel_sample_score(hw, prd, seg, c).cpu().numpy()
     assert np.array_equal(s, X[:, 58])
     assert np.all(X[:, 87] == 1) and np.all(X[:, 86] == 1)
+
+
+# ----------------------------------------------------------------------------
+# fused selection: features -> bins -> forest -> top-k in one call
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "medium", "dataset"])
+def test_fused_selection(name):
+    from _gpu_util import check_selection
+    say(f"fused selection {name}")
+    w = synth.workload(name)
+    cfg = w.cfg
+    d = Dev(w)
+    packed = hwsel.hwsel_forest_pack(d.forest)
+    ws = torch.empty(hwsel.hwsel_forest_workspace_bytes(d.forest, cfg.rows), dtype=torch.uint8, device="cuda")
+    X = d.features(cfg.n_features)
+    s = hwsel.hwsel_forest_score(d.forest, X, packed=packed, workspace=ws)
+    idx, vals = hwsel.hwsel_topk_per_problem(s, d.seg, cfg.k)
+    del X
+    fs = torch.empty(cfg.rows, dtype=torch.float32, device="cuda")
+    fidx, fvals, _ = hwsel.hwsel_select_forest(w.hw, d.problems, d.seg, d.cands, cfg.n_features, d.forest, packed,
+                                               cfg.k, scores=fs)
+    assert bool((fs.view(torch.int32) == s.view(torch.int32)).all())
+    assert np.array_equal(fidx.cpu().numpy(), idx.cpu().numpy())
+    assert np.array_equal(fvals.cpu().numpy().view(np.uint32), vals.cpu().numpy().view(np.uint32))
+    # no scores requested: the workspace holds them
+    fidx2, _, _ = hwsel.hwsel_select_forest(w.hw, d.problems, d.seg, d.cands, cfg.n_features, d.forest, packed,
+                                            cfg.k, with_vals=False)
+    assert np.array_equal(fidx2.cpu().numpy(), idx.cpu().numpy())
+    probs = np.arange(cfg.n_problems) if name == "tiny" else \
+        np.random.default_rng(cfg.seed + 1).choice(cfg.n_problems, 2, replace=False)
+    check_selection(w, fidx.cpu().numpy(), probs)

@@ -17,7 +17,7 @@ import torch
 
 import oracle
 import synth
-from _gpu_util import Dev, assert_forest_scores, compare_features, path_l1, say
+from _gpu_util import Dev, assert_forest_scores, check_selection, compare_features, path_l1, say
 from paper_2609_35587_amd import hwsel
 
 pytestmark = pytest.mark.gpu
@@ -172,17 +172,22 @@ def test_forest_workload_full_size(name):
         sg = hwsel.hwsel_forest_score(pd, X)
         assert bool((sp == sg).all()), t0
     say("  packed leaf indices match for probed trees")
-    say(f"workload {name}: top-k / regret")
-    idx, vals = hwsel.hwsel_topk_per_problem(s, d.seg, cfg.k)
-    r1, rk, best = hwsel.hwsel_regret(d.runtimes, d.seg, idx)
-    s_host = s.cpu().numpy()
-    oidx, ovals = oracle.topk(s_host, w.seg, cfg.k)
-    assert np.array_equal(idx.cpu().numpy(), oidx)
+    say(f"workload {name}: end-to-end selection on sampled problems")
+    idx = hwsel.hwsel_topk_per_problem(s, d.seg, cfg.k, with_vals=False)[0].cpu().numpy()
+    check_selection(w, idx, np.random.default_rng(cfg.seed).choice(cfg.n_problems, 3, replace=False))
+    say(f"workload {name}: top-k / regret at full size on generator scores")
+    rng = np.random.default_rng(cfg.seed + 100)
+    s_gen = synth.random_scores(rng, cfg.rows, tie_frac=0.2, n_levels=64)
+    gidx, gvals = hwsel.hwsel_topk_per_problem(torch.from_numpy(s_gen).cuda(), d.seg, cfg.k)
+    oidx, ovals = oracle.topk(s_gen, w.seg, cfg.k)
+    assert np.array_equal(gidx.cpu().numpy(), oidx)
+    assert np.array_equal(gvals.cpu().numpy().view(np.uint32), ovals.view(np.uint32))
+    r1, rk, best = hwsel.hwsel_regret(d.runtimes, d.seg, torch.from_numpy(oidx).cuda())
     o1, ok, ob = oracle.regret(w.runtimes, w.seg, oidx)
     assert np.array_equal(r1.cpu().numpy().view(np.uint32), o1.view(np.uint32))
     assert np.array_equal(rk.cpu().numpy().view(np.uint32), ok.view(np.uint32))
     assert np.array_equal(best.cpu().numpy(), ob)
-    say(f"  mean regret top1 {np.nanmean(o1):.4f}")
+    say(f"  mean regret top1 of generator scores {np.nanmean(o1):.4f}")
 
 
 def _assert_mlp(g, o):
