@@ -13,7 +13,12 @@ Prints ONE JSON line (rank 0).  `value` = rows per second through the whole
 step.  Per-stage times come from HIP events recorded on the launch stream
 inside the timed region.  `roofline` is for the dominant kernel (forest
 scoring); `cpu_baseline` times the CPU oracle on a bounded sample of the same
-workload on the host cores.
+workload on the host cores.  `extras` times, each on its own after the timed
+step, the entries around the path on the same workload: the fused
+features -> forest -> top-k selection, the linear and sampling-score scorers,
+the selection metrics and static-configuration baseline, and the
+configuration catalogue (mask, compaction, candidate rows) for the same 600
+problems.
 """
 from __future__ import annotations
 
@@ -80,6 +85,76 @@ def cpu_baseline(w, n_problems: int) -> dict:
                       f"(features, forest, MLP, top-{cfg.k}, regret), {dt:.1f} s"}
 
 
+def timed(torch, fn, reps: int = 3) -> float:
+    """Median milliseconds of fn() over reps runs (HIP events on the current
+    stream), after one untimed run."""
+    fn()
+    stream = torch.cuda.current_stream()
+    out = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1))
+    return float(np.median(out))
+
+
+def extras(a, w, hwsel, torch, dev, probs, seg, cands, rt, forest, packed, X, idx, per_stage) -> dict:
+    """Entries around the scored path on the same workload, each timed on its
+    own (outside the timed step): the fused selection, the cheap scorers, the
+    selection metrics and baselines, and the configuration catalogue."""
+    import synth
+    cfg = w.cfg
+    R, P, F, k = cfg.rows, cfg.n_problems, cfg.n_features, cfg.k
+    out = {}
+    log("extras: fused selection")
+    wsf = torch.empty(hwsel.hwsel_select_forest_workspace_bytes(forest, R), dtype=torch.uint8, device=dev)
+    fidx = torch.empty((P, k), dtype=torch.int32, device=dev)
+    ms = timed(torch, lambda: hwsel.hwsel_select_forest(w.hw, probs, seg, cands, F, forest, packed, k,
+                                                        workspace=wsf, idx=fidx, with_vals=False))
+    unfused = per_stage["features"] + per_stage["forest"] + per_stage["topk_forest"]
+    out["fused_selection"] = {"ms": ms, "rows_per_s": R / (ms / 1e3), "unfused_ms": unfused,
+                              "same_choice": bool(torch.equal(fidx, idx))}
+    del wsf
+    log("extras: linear and sampling scorers")
+    lin = {kk: (hwsel.to_device(v, dev) if isinstance(v, np.ndarray) else v) for kk, v in synth.linear(cfg).items()}
+    sl = torch.empty(R, dtype=torch.float32, device=dev)
+    ms = timed(torch, lambda: hwsel.hwsel_linear_score(lin, X, scores=sl))
+    gbs = R * (4 * F + 4) / (ms / 1e3) / 1e9
+    out["linear_score"] = {"ms": ms, "rows_per_s": R / (ms / 1e3), "GBps": gbs, "hbm_frac": gbs / HBM_PEAK_GBS,
+                           "bytes_per_row": 4 * F + 4}
+    ms = timed(torch, lambda: hwsel.hwsel_sample_score(w.hw, probs, seg, cands, scores=sl))
+    gbs = R * 21 / (ms / 1e3) / 1e9
+    out["sample_score"] = {"ms": ms, "rows_per_s": R / (ms / 1e3), "GBps": gbs, "hbm_frac": gbs / HBM_PEAK_GBS,
+                           "bytes_per_row": 21}
+    log("extras: metrics and baselines")
+    ms = timed(torch, lambda: hwsel.hwsel_evaluate(rt, seg, idx, per_group=False))
+    gbs = R * 4 / (ms / 1e3) / 1e9
+    out["evaluate"] = {"ms": ms, "GBps": gbs, "hbm_frac": gbs / HBM_PEAK_GBS, "problems": P}
+    ids = hwsel.to_device(w.extra["config_id"], dev)
+    n_cfg = int(w.extra["config_id"].max()) + 1
+    ms = timed(torch, lambda: hwsel.hwsel_static_config(rt, seg, ids, n_cfg))
+    out["static_config"] = {"ms": ms, "configs": n_cfg, "problems": P}
+    log("extras: catalogue")
+    mask = torch.empty((P, hwsel.HWSEL_CATALOGUE_SIZE), dtype=torch.uint8, device=dev)
+    ms_mask = timed(torch, lambda: hwsel.hwsel_catalogue_mask(w.hw, probs, 1, mask=mask))
+    _, n_valid = hwsel.hwsel_catalogue_mask(w.hw, probs, 1, mask=mask)
+    total = int(n_valid.sum().item())
+    pt = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
+    ms_comp = timed(torch, lambda: hwsel.hwsel_catalogue_compact(mask, n_valid, total, point=pt))
+    cseg, _ = hwsel.hwsel_catalogue_compact(mask, n_valid, total, point=pt)
+    ms_rows = timed(torch, lambda: hwsel.hwsel_catalogue_candidates(probs, cseg, total, point=pt))
+    mbytes = P * hwsel.HWSEL_CATALOGUE_SIZE
+    out["catalogue"] = {"problems": P, "points_per_problem": hwsel.HWSEL_CATALOGUE_SIZE, "valid_rows": total,
+                        "mask_ms": ms_mask, "mask_points_per_s": mbytes / (ms_mask / 1e3),
+                        "mask_hbm_frac": mbytes / (ms_mask / 1e3) / 1e9 / HBM_PEAK_GBS,
+                        "compact_ms": ms_comp, "candidates_ms": ms_rows}
+    del mask, pt
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -88,6 +163,9 @@ def main():
     ap.add_argument("--cpu-problems", type=int, default=64,
                     help="problems in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the separately timed entries around the path (fused selection, cheap scorers, "
+                         "metrics, catalogue)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="run one plain 1 GiB device-to-device copy before the timed region (a known-size "
                          "reference for the HBM byte counters)")
@@ -202,6 +280,9 @@ def main():
                      "visits_per_launch": visits,
                      "hbm_frac": forest_bytes / t_forest / 1e9 / HBM_PEAK_GBS},
     }
+    if not a.no_extras:
+        line["extras"] = extras(a, w, hwsel, torch, dev, probs, seg, cands, rt, forest, packed, X, outs[0][0],
+                                per_stage)
     if not a.no_cpu_baseline:
         log(f"cpu baseline: oracle on {a.cpu_problems} problems")
         line["cpu_baseline"] = cpu_baseline(w, a.cpu_problems)

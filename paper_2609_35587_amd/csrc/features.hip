@@ -292,6 +292,7 @@ __global__ __launch_bounds__(256) void k_sample_score(HwDev h, const hwsel_probl
 constexpr int kFbThreads = 256;
 constexpr int kFbSlots = 256;
 constexpr int kFbStride = 257;
+constexpr int kFbChains = 32;
 
 template <int F>
 __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const hwsel_problem_t *__restrict__ probs,
@@ -311,15 +312,24 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
         uint32_t word[F / 4];
 #pragma unroll
         for (int q = 0; q < F / 4; ++q) word[q] = 0;
+        // kFbChains independent searches in flight
 #pragma unroll
-        for (int f = 0; f < F; ++f) {
-            if (f < nf) {
-                const float *uf = u + f * kFbStride;
-                uint32_t b = 0;
+        for (int f0 = 0; f0 < F; f0 += kFbChains) {
+            if (f0 < nf) {
+                uint32_t b[kFbChains];
 #pragma unroll
-                for (int step = 128; step > 0; step >>= 1) b += (uf[b + step - 1] <= x[f]) ? step : 0;
-                if (x[f] != x[f]) b = nan_bin;
-                word[f / 4] |= b << (8 * (f % 4));
+                for (int q = 0; q < kFbChains; ++q) b[q] = (uint32_t)(f0 + q) * kFbStride;
+#pragma unroll
+                for (int step = 128; step > 0; step >>= 1)
+#pragma unroll
+                    for (int q = 0; q < kFbChains; ++q) b[q] += (u[b[q] + step - 1] <= x[f0 + q]) ? step : 0;
+#pragma unroll
+                for (int q = 0; q < kFbChains; ++q) {
+                    uint32_t v = b[q] - (uint32_t)(f0 + q) * kFbStride;
+                    if (x[f0 + q] != x[f0 + q]) v = nan_bin;
+                    if (f0 + q >= nf) v = 0;
+                    word[(f0 + q) / 4] |= v << (8 * ((f0 + q) % 4));
+                }
             }
         }
         uint8_t *dst = Xb + r * stride;
