@@ -674,7 +674,8 @@ int oracle_linear(const o_linear *m, const float *X, int64_t ld, int64_t n, floa
 /* Per group g with candidates c and runtimes t_c (throughput ~ 1/t at a    */
 /* fixed flop count, so y(g,c) = T(c) / T_best = t_best / t_c):            */
 /*   t_best   minimum runtime (NaN ranks above +inf),                        */
-/*   R(g)     = 1 - t_best / t(c_hat), c_hat = idx[g][0]; 0 when equal,    */
+/*   R(g)     = 1 - y(g, c_hat), c_hat = idx[g][0]  (1 - t_best / t(c_hat); */
+/*              0 when equal; 1 for a NaN runtime, read as never finishing), */
 /*   rank     = 1 + #{c : t_c faster than t(c_hat)}  (minimum-rank ties),   */
 /*   ybar(g)  = mean_c y(g,c), y = 1 when t_c == t_best, 0 when t_c is NaN  */
 /*              (and t_best is not), else t_best / t_c; random-pick regret  */
@@ -744,7 +745,7 @@ int oracle_evaluate(const float *rt, const int64_t *seg, int64_t P, const int32_
         yb[p] = ysum / (double)n;
         if (!counted[p]) continue;
         const float t_sel = rt[base + sel];
-        R[p] = t_sel == t_star ? 0.0 : 1.0 - (double)t_star / (double)t_sel;
+        R[p] = 1.0 - y_of(t_star, t_sel);
         int32_t better = 0;
         for (int64_t j = 0; j < n; ++j) better += faster64(rt[base + j], t_sel);
         rk[p] = 1 + better;
