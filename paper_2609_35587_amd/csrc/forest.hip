@@ -104,7 +104,9 @@ ForestDev to_dev(const hwsel_forest_t &f)
 // ---------------------------------------------------------------------------
 constexpr int kBinSlots = 256;        // thresholds per feature incl. padding
 constexpr int kBinStrideLds = 257;    // LDS row stride (floats) of the bin table
-constexpr int kTileRows = 256;        // rows of bins per LDS tile
+// Rows of bins per LDS tile: as many as fit next to a 96 KB tree chunk, in
+// whole groups per wave (more rows per wave = more walks in flight).
+__host__ __device__ constexpr int tile_rows(int tc) { return tc == 64 ? 384 : 448; }
 constexpr int kTileStride = 132;      // LDS bytes per bin row (33 dwords)
 constexpr int kWaves = 16;            // waves per traversal workgroup
 constexpr int kXcds = 8;
@@ -235,8 +237,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
     constexpr int NODE_B = NS * TC * 2;
     constexpr int CHUNK_B = NS * TC * 6;
     constexpr int RPI = 64 / TC;                       // rows per lane group
-    constexpr int ROWS_PER_WAVE = kTileRows / kWaves;  // 16
-    constexpr int ILP = ROWS_PER_WAVE / RPI < 8 ? ROWS_PER_WAVE / RPI : 8;   // row groups in flight
+    constexpr int kTileRows = tile_rows(TC);
+    constexpr int ROWS_PER_WAVE = kTileRows / kWaves;  // 24 or 28
+    constexpr int GROUPS = ROWS_PER_WAVE / RPI;
+    constexpr int ILP = GROUPS % 8 == 0 ? 8 : GROUPS % 7 == 0 ? 7 : GROUPS % 6 == 0 ? 6 : 4;   // groups in flight
     constexpr int ITER = ROWS_PER_WAVE / (RPI * ILP);
     static_assert(ITER >= 1 && ITER * RPI * ILP == ROWS_PER_WAVE, "tile shape");
     __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kTileStride + kTileRows * 4];
@@ -265,7 +269,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
         }
         // Bin tiles stream through registers: tile k+1 is fetched from global
         // memory while tile k is walked from LDS.
-        constexpr int kVec = kTileRows * 128 / 16 / (64 * kWaves);   // uint4 per thread (2)
+        constexpr int kVec = (kTileRows * 128 / 16 + 64 * kWaves - 1) / (64 * kWaves);   // uint4 per thread
         const int vpr = stride >> 4;                                  // uint4 per bin row
         uint4 pre[kVec];
         auto fetch = [&](int64_t t0) {
@@ -341,7 +345,7 @@ hipError_t launch_traverse_tc(const uint8_t *chunks, int n_chunks, const uint8_t
     const int groups = n_chunks >= kSlotsPerXcd ? 1 : (kSlotsPerXcd + n_chunks - 1) / n_chunks;
     const int64_t n_groups = (int64_t)kXcds * groups;
     int64_t per = (R + n_groups - 1) / n_groups;
-    per = (per + kTileRows - 1) / kTileRows * kTileRows;
+    per = (per + tile_rows(TC) - 1) / tile_rows(TC) * tile_rows(TC);
     hipLaunchKernelGGL((k_traverse<TC, D>), dim3(kXcds * kSlotsPerXcd), dim3(64 * kWaves), 0, s, chunks,
                        n_chunks, Xb, R, stride, groups, per, partial);
     return hipGetLastError();
