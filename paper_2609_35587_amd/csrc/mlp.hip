@@ -18,10 +18,11 @@
 //     16 bytes of one activation row from LDS; the accumulator tile gives each
 //     lane 4 runs of 4 consecutive units of one row.
 //   * Waves split the output units of a layer, so every weight is read once
-//     per tile; a layer's results wait in registers until all waves have
-//     read the previous layer, then overwrite it in place.  While a wave's
-//     second block of products runs on the matrix core, the vector units
-//     finish the first block's epilogue.
+//     per tile; in a 512-unit layer a wave's two M-tiles share every
+//     activation fragment read.  A layer's results wait in registers until
+//     all waves have read the previous layer, then overwrite it in place.
+//     In the last layer the first block's epilogue runs on the vector units
+//     while the second block's products run on the matrix core.
 //   * GELU(a) = a/2 (1 + erf(a / sqrt 2)) with erf from Abramowitz & Stegun
 //     7.1.28 (|error| <= 3e-7, far below the bf16 rounding that follows).
 //   * The 256 -> 1 layer is a dot product folded into layer 3's epilogue,
@@ -296,6 +297,63 @@ __device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const u
     }
 }
 
+// acc[mt][nt] = init[mt] + products of the wave's two consecutive M-tiles
+// (fragments at W0 and W0 + KS fragments) with 4 N-tiles: every activation
+// fragment read serves two products and every weight fragment four.  The
+// ring holds both M-tiles' fragments of two k-steps; each k-step's pair is
+// refilled with the k-step two ahead once its reads have returned.
+template <int K_IN>
+__device__ __forceinline__ void mma_block_mt2(const bf16x8 *__restrict__ W0, const uint8_t *act, int row_bytes,
+                                              int lane, uint32_t ring, const uint8_t *ring_ptr,
+                                              const f32x16 &init0, const f32x16 &init1, f32x16 (&acc)[2][4])
+{
+    constexpr int KS = K_IN / 16;
+    static_assert(KS % 2 == 0, "k loop");
+    const uint8_t *brow = act + (lane & 31) * row_bytes;
+    const int sw = lane & 15, half = lane >> 5;
+    const bf16x8 *w0 = W0 + lane, *w1 = W0 + KS * 64 + lane;
+    auto step = [&](int slot, int ks, bool first) {
+        const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
+        const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(ring_ptr + (slot + 1) * 1024 + lane * 16);
+        const int chunk = (((2 * ks + half) ^ sw) & 15) | ((2 * ks + half) & ~15);
+        bf16x8 b[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+            b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            acc[0][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b[nt], first ? init0 : acc[0][nt], 0, 0, 0);
+            acc[1][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b[nt], first ? init1 : acc[1][nt], 0, 0, 0);
+        }
+    };
+    auto refill = [&](int slot, int ks_next) {
+        if (ks_next < KS) {
+            reads_done();
+            dma_fragment(w0 + ks_next * 64, ring + slot * 1024);
+            dma_fragment(w1 + ks_next * 64, ring + (slot + 1) * 1024);
+            fragments_landed<2>();
+        } else {
+            fragments_landed<0>();
+        }
+    };
+    dma_fragment(w0, ring);
+    dma_fragment(w1, ring + 1024);
+    dma_fragment(w0 + 64, ring + 2048);
+    dma_fragment(w1 + 64, ring + 3072);
+    fragments_landed<2>();
+    step(0, 0, true);
+    refill(0, 2);
+    step(2, 1, false);
+    refill(2, 3);
+#pragma unroll 1
+    for (int ks = 2; ks < KS; ks += 2) {
+        step(0, ks, false);
+        refill(0, ks + 2);
+        step(2, ks + 1, false);
+        refill(2, ks + 3);
+    }
+}
+
 // Bias of one 32-unit M-tile starting at unit u0, in accumulator layout.
 __device__ __forceinline__ f32x16 bias_tile(const float *__restrict__ bias, int u0, int lane)
 {
@@ -330,22 +388,18 @@ __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const f
                                           const uint8_t *ring_ptr)
 {
     constexpr int KS = K_IN / 16;
-    constexpr int H = K_IN / 32;                  // side slots of a block
     uint2 staged[2][4][4];
-    f32x16 acc0[4], acc1[4];
-    mma_block<K_IN, 4>(Wf + (int64_t)(2 * wave) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr,
-                       bias_tile(bias, 64 * wave, lane), acc0);
-    // second M-tile; the first one's 16 epilogue groups ride along
-    mma_block<K_IN, 4, true>(Wf + (int64_t)(2 * wave + 1) * KS * 64, act, in_row_bytes, 0, lane, ring, ring_ptr,
-                             bias_tile(bias, 64 * wave + 32, lane), acc1, [&](int h) {
+    {
+        f32x16 acc[2][4];
+        mma_block_mt2<K_IN>(Wf + (int64_t)(2 * wave) * KS * 64, act, in_row_bytes, lane, ring, ring_ptr,
+                            bias_tile(bias, 64 * wave, lane), bias_tile(bias, 64 * wave + 32, lane), acc);
 #pragma unroll
-                                 for (int q = h * 16 / H; q < (h + 1) * 16 / H; ++q)
-                                     staged[0][q & 3][q >> 2] = gelu_group(acc0[q & 3], q >> 2);
-                             });
+        for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
+            for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) staged[1][nt][g] = gelu_group(acc1[nt], g);
+                for (int nt = 0; nt < 4; ++nt) staged[mt][nt][g] = gelu_group(acc[mt][nt], g);
+    }
     __syncthreads();
     // Lanes l and l + 32 hold the two halves of each 16-byte chunk; one
     // cross-half swap per register gives lane l (l < 32) chunk g = 2p and
