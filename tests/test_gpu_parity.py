@@ -248,3 +248,39 @@ def test_mlp_ragged_and_nonfinite(R):
     _assert_mlp(g, o)
     g2 = hwsel.hwsel_mlp_score(md, Xd).cpu().numpy()
     _assert_mlp(g2, o)
+
+
+# ----------------------------------------------------------------------------
+# every packed traversal shape (depth 1..10, chunk widths 64/32/16), padding
+# trees, ragged row counts, NaN features with both default directions
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("depth,trees,flags", [(1, 1, 1), (2, 65, 0), (3, 64, 1), (4, 7, 1), (5, 130, 0),
+                                               (6, 33, 1), (7, 64, 0), (8, 70, 1), (9, 33, 1), (9, 40, 0),
+                                               (10, 17, 1), (10, 20, 0)])
+def test_forest_every_depth(depth, trees, flags):
+    import dataclasses
+    say(f"forest depth {depth} trees {trees} flags {flags}")
+    base = synth.CONFIGS["tiny"]
+    cfg = dataclasses.replace(base, trees=trees, depth=depth)
+    w = synth.workload("tiny", with_model=False)
+    f = synth.forest(cfg)
+    f["flags"] = flags
+    R = 8191
+    X = oracle.features(w.hw, w.problems, w.seg, w.cands, 64)[:R].copy()
+    rng = np.random.default_rng(depth * 100 + trees)
+    X[rng.random(X.shape) < 0.02] = np.nan
+    o, oli = oracle.forest(f, X, leaves=True)
+    l1 = path_l1(f, oli)
+    from _gpu_util import forest_to_device
+    fd = forest_to_device(f)
+    Xd = torch.from_numpy(X).cuda()
+    g = hwsel.hwsel_forest_score(fd, Xd).cpu().numpy()
+    e_direct = assert_forest_scores(g, o, l1)
+    packed = hwsel.hwsel_forest_pack(fd)
+    ws = torch.empty(hwsel.hwsel_forest_workspace_bytes(fd, R), dtype=torch.uint8, device="cuda")
+    gp = hwsel.hwsel_forest_score(fd, Xd, packed=packed, workspace=ws).cpu().numpy()
+    e_packed = assert_forest_scores(gp, o, l1)
+    rows = torch.arange(0, R, 7, dtype=torch.int64, device="cuda")
+    li = hwsel.hwsel_forest_leaves(fd, Xd, rows).cpu().numpy().view(np.uint16)
+    assert np.array_equal(li, oli[::7])
+    say(f"  err/bound direct {e_direct:.3g} packed {e_packed:.3g}")
