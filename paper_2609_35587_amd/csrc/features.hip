@@ -227,6 +227,11 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
 
 constexpr int kWaves = 4;
 
+// One row per thread.  The row's columns are produced 64 (or 32) at a time:
+// each pass evaluates the feature map and keeps only its columns (the shared
+// integer intermediates are recomputed, the per-column work is not), which
+// keeps the live registers low enough for more than one wave per SIMD.  Each
+// 32-column slab is transposed through LDS into 16-byte row stores.
 template <int F>
 __global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_problem_t *__restrict__ probs,
                                                           int32_t P, const int64_t *__restrict__ seg,
@@ -237,19 +242,25 @@ __global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_p
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t row0 = ((int64_t)blockIdx.x * kWaves + wave) * 64;
     const int64_t r = row0 + lane;
-    float x[F];
-    if (r < R) {
-        const int32_t p = segment_of_row(seg, P, r);
-        const hwsel_problem_t pb = probs[p];
-        phi<F>(h, pb, c, r, x);
-    } else {
-#pragma unroll
-        for (int j = 0; j < F; ++j) x[j] = 0.0f;
-    }
+    hwsel_problem_t pb{};
+    if (r < R) pb = probs[segment_of_row(seg, P, r)];
+    constexpr int kPass = F % 64 == 0 ? 64 : 32;      // columns per evaluation of the map
+    float xs[kPass];
 #pragma unroll
     for (int ch = 0; ch < F / 32; ++ch) {
+        if (ch % (kPass / 32) == 0) {
+            float x[F];
+            if (r < R) {
+                phi<F>(h, pb, c, r, x);
+            } else {
 #pragma unroll
-        for (int j = 0; j < 32; ++j) stage[wave][lane][j] = x[ch * 32 + j];
+                for (int j = 0; j < F; ++j) x[j] = 0.0f;
+            }
+#pragma unroll
+            for (int j = 0; j < kPass; ++j) xs[j] = x[ch * 32 + j];
+        }
+#pragma unroll
+        for (int j = 0; j < 32; ++j) stage[wave][lane][j] = xs[(ch % (kPass / 32)) * 32 + j];
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -289,10 +300,10 @@ __global__ __launch_bounds__(256) void k_sample_score(HwDev h, const hwsel_probl
 // sorted thresholds (b = #{u : u <= x}, NaN to nan_bin), the same search as
 // the forest's own binning pass; X is never written.  One workgroup per CU
 // holds the threshold table in LDS and walks row tiles.
-constexpr int kFbThreads = 256;
+constexpr int kFbThreads = 512;
 constexpr int kFbSlots = 256;
 constexpr int kFbStride = 257;
-constexpr int kFbChains = 32;
+constexpr int kFbChains = 8;
 
 template <int F>
 __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const hwsel_problem_t *__restrict__ probs,
@@ -304,31 +315,41 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
     __shared__ float u[128 * kFbStride];
     for (int e = threadIdx.x; e < nf * kFbSlots; e += kFbThreads) u[(e >> 8) * kFbStride + (e & 255)] = U[e];
     __syncthreads();
+    constexpr int kPass = F % 64 == 0 ? 64 : 32;      // columns per evaluation of the map
     for (int64_t r = (int64_t)blockIdx.x * kFbThreads + threadIdx.x; r < R; r += (int64_t)gridDim.x * kFbThreads) {
-        float x[F];
         const int32_t p = segment_of_row(seg, P, r);
         const hwsel_problem_t pb = probs[p];
-        phi<F>(h, pb, c, r, x);
         uint32_t word[F / 4];
 #pragma unroll
         for (int q = 0; q < F / 4; ++q) word[q] = 0;
-        // kFbChains independent searches in flight
 #pragma unroll
-        for (int f0 = 0; f0 < F; f0 += kFbChains) {
-            if (f0 < nf) {
-                uint32_t b[kFbChains];
+        for (int p0 = 0; p0 < F; p0 += kPass) {
+            if (p0 >= nf) break;
+            // an opaque copy of the row index keeps each pass's evaluation
+            // separate (otherwise the passes are merged into one evaluation
+            // with every column live)
+            int64_t rp = r;
+            asm volatile("" : "+v"(rp));
+            float x[F];
+            phi<F>(h, pb, c, rp, x);
+            // kFbChains independent searches in flight
 #pragma unroll
-                for (int q = 0; q < kFbChains; ++q) b[q] = (uint32_t)(f0 + q) * kFbStride;
+            for (int f0 = p0; f0 < p0 + kPass; f0 += kFbChains) {
+                if (f0 < nf) {
+                    uint32_t b[kFbChains];
 #pragma unroll
-                for (int step = 128; step > 0; step >>= 1)
+                    for (int q = 0; q < kFbChains; ++q) b[q] = (uint32_t)(f0 + q) * kFbStride;
 #pragma unroll
-                    for (int q = 0; q < kFbChains; ++q) b[q] += (u[b[q] + step - 1] <= x[f0 + q]) ? step : 0;
+                    for (int step = 128; step > 0; step >>= 1)
 #pragma unroll
-                for (int q = 0; q < kFbChains; ++q) {
-                    uint32_t v = b[q] - (uint32_t)(f0 + q) * kFbStride;
-                    if (x[f0 + q] != x[f0 + q]) v = nan_bin;
-                    if (f0 + q >= nf) v = 0;
-                    word[(f0 + q) / 4] |= v << (8 * ((f0 + q) % 4));
+                        for (int q = 0; q < kFbChains; ++q) b[q] += (u[b[q] + step - 1] <= x[f0 + q]) ? step : 0;
+#pragma unroll
+                    for (int q = 0; q < kFbChains; ++q) {
+                        uint32_t v = b[q] - (uint32_t)(f0 + q) * kFbStride;
+                        if (x[f0 + q] != x[f0 + q]) v = nan_bin;
+                        if (f0 + q >= nf) v = 0;
+                        word[(f0 + q) / 4] |= v << (8 * ((f0 + q) % 4));
+                    }
                 }
             }
         }
