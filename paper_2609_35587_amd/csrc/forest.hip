@@ -157,7 +157,7 @@ __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict_
     const int sub = threadIdx.x >> 7;                 // 8 row lanes per block
     if (f >= stride) return;
     const float *uf = u + f * kBinStrideLds;
-    constexpr int kRowsPerThread = 4;                 // independent searches in flight
+    constexpr int kRowsPerThread = 8;                 // independent searches in flight
     const int64_t step_rows = (int64_t)gridDim.x * 8 * kRowsPerThread;
     for (int64_t r0 = ((int64_t)blockIdx.x * 8 + sub) * kRowsPerThread; r0 < R; r0 += step_rows) {
         float x[kRowsPerThread];
