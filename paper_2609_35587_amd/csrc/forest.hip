@@ -338,6 +338,25 @@ __global__ __launch_bounds__(256) void k_reduce(const float *__restrict__ partia
     scores[r] = acc;
 }
 
+// Four rows per thread with 16-byte loads (R % 4 == 0, so every chunk's
+// partial row starts 16-byte aligned); same chunk order per row.
+__global__ __launch_bounds__(256) void k_reduce4(const float *__restrict__ partial, int n_chunks, int64_t R,
+                                                  float base, float *__restrict__ scores)
+{
+    const int64_t r = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+    if (r >= R) return;
+    float4 acc = make_float4(base, base, base, base);
+#pragma unroll 8
+    for (int c = 0; c < n_chunks; ++c) {
+        const float4 v = *reinterpret_cast<const float4 *>(partial + (int64_t)c * R + r);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+    }
+    *reinterpret_cast<float4 *>(scores + r) = acc;
+}
+
 template <int TC, int D>
 hipError_t launch_traverse_tc(const uint8_t *chunks, int n_chunks, const uint8_t *Xb, int64_t R, int stride,
                               float *partial, hipStream_t s)
@@ -494,8 +513,12 @@ hipError_t launch_forest_from_bins(const hwsel_forest_t &f, const void *packed, 
     float *partial = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + align256((size_t)R * g.stride));
     hipError_t e = launch_traverse(f.depth, chunks, g.n_chunks, Xb, R, g.stride, partial, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_reduce, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
-                       f.base_score, scores);
+    if (R % 4 == 0 && ((uintptr_t)scores & 15u) == 0)
+        hipLaunchKernelGGL(k_reduce4, dim3((unsigned)((R / 4 + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
+                           f.base_score, scores);
+    else
+        hipLaunchKernelGGL(k_reduce, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
+                           f.base_score, scores);
     return hipGetLastError();
 }
 
