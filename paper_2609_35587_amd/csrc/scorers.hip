@@ -2,10 +2,10 @@
 //   f(x) = bias + sum_j w_j (clean(x_j) - mean_j) inv_std_j + one-hot terms.
 //
 // The pass is a GEMV over X and is bound by reading X from HBM (512 bytes per
-// 128-column row, 4 bytes out).  A wave reads two rows per step with 16-byte
-// loads, each lane taking four consecutive columns; the per-lane partial sums
-// of a row are combined by a fixed butterfly over its 32 lanes, so the result
-// does not depend on scheduling.
+// 128-column row, 4 bytes out).  Each 16-byte load of a wave covers two rows,
+// each lane taking four consecutive columns, and four such loads are in
+// flight per lane; the per-lane partial sums of a row are combined by a fixed
+// butterfly over its 32 lanes, so the result does not depend on scheduling.
 #include "internal.hpp"
 
 namespace hwsel {
@@ -58,19 +58,29 @@ __global__ __launch_bounds__(64 * kLinWaves) void k_linear(hwsel_linear_t lin, c
     const bool active = c0 < lin.n_features;
     const int64_t pairs = (R + 1) / 2;
     const int64_t stride = (int64_t)gridDim.x * kLinWaves;
-    for (int64_t pr = (int64_t)blockIdx.x * kLinWaves + (threadIdx.x >> 6); pr < pairs; pr += stride) {
-        const int64_t r = 2 * pr + (lane >> 5);
-        float acc = 0.0f;
-        if (r < R && active) {
-            const float4 v = *reinterpret_cast<const float4 *>(X + r * ld + c0);
-            acc = term(t[0], v.x, lin.w_onehot);
-            acc += term(t[1], v.y, lin.w_onehot);
-            acc += term(t[2], v.z, lin.w_onehot);
-            acc += term(t[3], v.w, lin.w_onehot);
+    constexpr int kIn = 4;     // row pairs per wave step: four 16-byte loads in flight per lane
+    for (int64_t pr0 = (int64_t)blockIdx.x * kLinWaves + (threadIdx.x >> 6); pr0 < pairs; pr0 += kIn * stride) {
+        float4 v[kIn];
+#pragma unroll
+        for (int i = 0; i < kIn; ++i) {
+            const int64_t r = 2 * (pr0 + i * stride) + (lane >> 5);
+            v[i] = (r < R && active) ? *reinterpret_cast<const float4 *>(X + r * ld + c0)
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
-        for (int o = 16; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 32);
-        if ((lane & 31) == 0 && r < R) scores[r] = acc + lin.bias;
+        for (int i = 0; i < kIn; ++i) {
+            const int64_t r = 2 * (pr0 + i * stride) + (lane >> 5);
+            float acc = 0.0f;
+            if (r < R && active) {
+                acc = term(t[0], v[i].x, lin.w_onehot);
+                acc += term(t[1], v[i].y, lin.w_onehot);
+                acc += term(t[2], v[i].z, lin.w_onehot);
+                acc += term(t[3], v[i].w, lin.w_onehot);
+            }
+#pragma unroll
+            for (int o = 16; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 32);
+            if ((lane & 31) == 0 && r < R) scores[r] = acc + lin.bias;
+        }
     }
 }
 
