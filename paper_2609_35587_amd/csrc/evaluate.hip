@@ -112,34 +112,97 @@ __global__ __launch_bounds__(kEvalThreads) void k_eval_groups(const float *__res
     }
 }
 
-// sorted[position of problem i among counted regrets] = regret[i]; the
-// position counts smaller values and equal values of lower index.
-__global__ __launch_bounds__(kEvalThreads) void k_eval_order(const double *__restrict__ regret,
-                                                             const int32_t *__restrict__ rank, int32_t P,
-                                                             double *__restrict__ sorted)
+// Order statistics of the counted regrets by radix selection: for each
+// requested rank, eight passes over the 64-bit keys (an order-preserving map
+// of the binary64 values), one byte per pass from the top, each counting the
+// candidates that still match the prefix.  Linear in P per pass; the counts
+// are integers, so the result is exact and independent of scheduling.
+// stats[i] = the value of rank ranks[i] (0-based) among the counted regrets,
+// for the ranks of the median and the 95th percentile.
+__device__ __forceinline__ uint64_t order_key(double v)
 {
-    const int32_t i = blockIdx.x * kEvalThreads + threadIdx.x;
-    if (i >= P || rank[i] == 0) return;
-    const double v = regret[i];
-    int64_t pos = 0;
-    for (int32_t j = 0; j < P; ++j) {
-        if (rank[j] == 0) continue;
-        const double u = regret[j];
-        pos += (u < v || (u == v && j < i)) ? 1 : 0;
-    }
-    sorted[pos] = v;
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
 }
 
-__device__ double percentile(const double *s, int64_t n, double q)
+__device__ __forceinline__ double key_value(uint64_t k)
+{
+    return __builtin_bit_cast(double, (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k);
+}
+
+constexpr int kSelectThreads = 1024;
+
+__global__ __launch_bounds__(kSelectThreads) void k_eval_select(const double *__restrict__ regret,
+                                                                const int32_t *__restrict__ rank, int32_t P,
+                                                                double *__restrict__ stats)
+{
+    __shared__ int64_t hist[256];
+    __shared__ int64_t cnt_s;
+    __shared__ uint64_t prefix_s;
+    __shared__ int64_t k_s;
+    // number of counted problems
+    if (threadIdx.x == 0) cnt_s = 0;
+    __syncthreads();
+    int64_t local = 0;
+    for (int32_t i = threadIdx.x; i < P; i += kSelectThreads) local += rank[i] != 0;
+    atomicAdd(reinterpret_cast<unsigned long long *>(&cnt_s), (unsigned long long)local);
+    __syncthreads();
+    const int64_t n = cnt_s;
+    if (n == 0) return;
+    // ranks: floor and ceil positions of q (n - 1) for q = 0.5, 0.95
+    int64_t want[4];
+    {
+        const double p50 = 0.5 * (double)(n - 1), p95 = 0.95 * (double)(n - 1);
+        const int64_t l50 = (int64_t)__builtin_floor(p50), l95 = (int64_t)__builtin_floor(p95);
+        want[0] = l50;
+        want[1] = l50 + 1 < n ? l50 + 1 : n - 1;
+        want[2] = l95;
+        want[3] = l95 + 1 < n ? l95 + 1 : n - 1;
+    }
+    for (int t = 0; t < 4; ++t) {
+        uint64_t prefix = 0, mask = 0;
+        int64_t k = want[t];
+        for (int shift = 56; shift >= 0; shift -= 8) {
+            for (int b = threadIdx.x; b < 256; b += kSelectThreads) hist[b] = 0;
+            __syncthreads();
+            for (int32_t i = threadIdx.x; i < P; i += kSelectThreads) {
+                if (rank[i] == 0) continue;
+                const uint64_t key = order_key(regret[i]);
+                if ((key & mask) == prefix)
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&hist[(key >> shift) & 255u]), 1ull);
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                int64_t acc = 0;
+                int d = 0;
+                for (; d < 255; ++d) {
+                    if (acc + hist[d] > k) break;
+                    acc += hist[d];
+                }
+                k_s = k - acc;
+                prefix_s = prefix | ((uint64_t)d << shift);
+            }
+            __syncthreads();
+            prefix = prefix_s;
+            k = k_s;
+            mask |= 0xffull << shift;
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) stats[t] = key_value(prefix);
+    }
+}
+
+// value at position q (n - 1) by linear interpolation between its two
+// neighbouring order statistics
+__device__ double interpolate(double lo_v, double hi_v, int64_t n, double q)
 {
     const double pos = q * (double)(n - 1);
-    const int64_t lo = (int64_t)__builtin_floor(pos);
-    const int64_t hi = lo + 1 < n ? lo + 1 : n - 1;
-    return s[lo] + (pos - (double)lo) * (s[hi] - s[lo]);
+    const double lo = __builtin_floor(pos);
+    return lo_v + (pos - lo) * (hi_v - lo_v);
 }
 
 __global__ void k_eval_aggregate(const double *__restrict__ regret, const int32_t *__restrict__ rank,
-                                 const double *__restrict__ ybar, const double *__restrict__ sorted, int32_t P,
+                                 const double *__restrict__ ybar, const double *__restrict__ stats, int32_t P,
                                  double *__restrict__ out, double *__restrict__ regret_out,
                                  int32_t *__restrict__ rank_out, double *__restrict__ ybar_out)
 {
@@ -162,8 +225,8 @@ __global__ void k_eval_aggregate(const double *__restrict__ regret, const int32_
             out[8] = 0.0;
         } else {
             out[0] = sum / (double)cnt;
-            out[1] = percentile(sorted, cnt, 0.5);
-            out[2] = percentile(sorted, cnt, 0.95);
+            out[1] = interpolate(stats[0], stats[1], cnt, 0.5);
+            out[2] = interpolate(stats[2], stats[3], cnt, 0.95);
             out[3] = mx;
             out[4] = (double)top1 / (double)cnt;
             out[5] = (double)top5 / (double)cnt;
@@ -284,12 +347,11 @@ hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const
     uint8_t *w = static_cast<uint8_t *>(ws);
     double *regret = reinterpret_cast<double *>(w);
     double *ybar = reinterpret_cast<double *>(w + up256((size_t)P * 8));
-    double *sorted = reinterpret_cast<double *>(w + 2 * up256((size_t)P * 8));
+    double *stats = reinterpret_cast<double *>(w + 2 * up256((size_t)P * 8));
     int32_t *rank = reinterpret_cast<int32_t *>(w + 3 * up256((size_t)P * 8));
     hipLaunchKernelGGL(k_eval_groups, dim3(P), dim3(kEvalThreads), 0, s, rt, seg, P, idx, k, regret, rank, ybar);
-    hipLaunchKernelGGL(k_eval_order, dim3((P + kEvalThreads - 1) / kEvalThreads), dim3(kEvalThreads), 0, s, regret,
-                       rank, P, sorted);
-    hipLaunchKernelGGL(k_eval_aggregate, dim3(1), dim3(256), 0, s, regret, rank, ybar, sorted, P, out, regret_out,
+    hipLaunchKernelGGL(k_eval_select, dim3(1), dim3(kSelectThreads), 0, s, regret, rank, P, stats);
+    hipLaunchKernelGGL(k_eval_aggregate, dim3(1), dim3(256), 0, s, regret, rank, ybar, stats, P, out, regret_out,
                        rank_out, ybar_out);
     return hipGetLastError();
 }

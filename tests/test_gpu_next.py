@@ -269,3 +269,14 @@ def test_fused_selection(name):
     probs = np.arange(cfg.n_problems) if name == "tiny" else \
         np.random.default_rng(cfg.seed + 1).choice(cfg.n_problems, 2, replace=False)
     check_selection(w, fidx.cpu().numpy(), probs)
+
+
+def test_evaluate_many_problems():
+    """Order statistics over many problems (radix selection, linear in P)."""
+    say("evaluate 50,000 problems")
+    rng = np.random.default_rng(11)
+    seg = synth.ragged_segments(rng, 50000, 12, empty_frac=0.05)
+    R = int(seg[-1])
+    rt = rng.choice(np.array([1.0, 1.25, 1.5, 2.0, 4.0, np.inf], np.float32), R)
+    idx, _ = oracle.topk(rng.standard_normal(R).astype(np.float32), seg, 1)
+    eval_compare(rt, seg, idx)
