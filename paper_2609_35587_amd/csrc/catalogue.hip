@@ -24,16 +24,19 @@ struct Knobs {
     int32_t tm, tn, tk, st, cm, cn, ks, es, ts;
 };
 
-__device__ __forceinline__ Knobs decode(int64_t i)
+// Point index -> knobs (the index fits in 32 bits, so the divisions by
+// constants are 32-bit multiply-shifts).
+__device__ __forceinline__ Knobs decode(int64_t index)
 {
+    uint32_t i = (uint32_t)index;
     Knobs k;
-    k.ts = (int32_t)(i % 2); i /= 2;
-    k.es = (int32_t)(i % 3); i /= 3;
-    k.ks = (int32_t)(i % 3); i /= 3;
-    const int32_t cl = (int32_t)(i % 15); i /= 15;
-    k.st = 2 + (int32_t)(i % 11); i /= 11;
-    k.tk = kTileK[i % 5]; i /= 5;
-    k.tn = kTileN[i % 9]; i /= 9;
+    k.ts = (int32_t)(i % 2u); i /= 2u;
+    k.es = (int32_t)(i % 3u); i /= 3u;
+    k.ks = (int32_t)(i % 3u); i /= 3u;
+    const uint32_t cl = i % 15u; i /= 15u;
+    k.st = 2 + (int32_t)(i % 11u); i /= 11u;
+    k.tk = kTileK[i % 5u]; i /= 5u;
+    k.tn = kTileN[i % 9u]; i /= 9u;
     k.tm = kTileM[i];
     k.cm = kClusterM[cl];
     k.cn = kClusterN[cl];
