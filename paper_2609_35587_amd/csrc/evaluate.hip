@@ -242,6 +242,88 @@ __global__ void k_eval_aggregate(const double *__restrict__ regret, const int32_
     }
 }
 
+// Up to kSmallP problems: one workgroup stages the per-problem values in LDS,
+// sorts the counted regrets with a bitonic network, and takes the sums in
+// problem order from LDS; the same outputs as k_eval_select +
+// k_eval_aggregate.
+constexpr int kSmallP = 4096;
+
+__global__ __launch_bounds__(1024) void k_eval_small(const double *__restrict__ regret,
+                                                     const int32_t *__restrict__ rank,
+                                                     const double *__restrict__ ybar, int32_t P,
+                                                     double *__restrict__ out, double *__restrict__ regret_out,
+                                                     int32_t *__restrict__ rank_out, double *__restrict__ ybar_out)
+{
+    __shared__ double reg_s[kSmallP], yb_s[kSmallP], sorted[kSmallP];
+    __shared__ int32_t rank_s[kSmallP];
+    for (int32_t i = threadIdx.x; i < kSmallP; i += 1024) {
+        const bool in = i < P;
+        reg_s[i] = in ? regret[i] : 0.0;
+        yb_s[i] = in ? ybar[i] : 0.0;
+        rank_s[i] = in ? rank[i] : 0;
+        sorted[i] = (in && rank[i] != 0) ? regret[i] : __builtin_inf();   // uncounted sort last
+    }
+    __syncthreads();
+    int32_t n2 = 1;
+    while (n2 < P) n2 <<= 1;
+    for (int32_t k = 2; k <= n2; k <<= 1)
+        for (int32_t j = k >> 1; j > 0; j >>= 1) {
+            for (int32_t i = threadIdx.x; i < n2; i += 1024) {
+                const int32_t l = i ^ j;
+                if (l > i) {
+                    const double a = sorted[i], b = sorted[l];
+                    const bool up = (i & k) == 0;
+                    if ((a > b) == up) {
+                        sorted[i] = b;
+                        sorted[l] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    if (threadIdx.x == 0) {
+        int64_t cnt = 0, top1 = 0, top5 = 0, w5 = 0;
+        double sum = 0.0, rsum = 0.0, mx = -__builtin_inf();
+        // Branch-free so the LDS reads pipeline: adding +0.0 for an
+        // uncounted problem leaves a sum that starts at +0.0 unchanged.
+#pragma unroll 8
+        for (int32_t p = 0; p < P; ++p) {
+            const int32_t rk = rank_s[p];
+            const bool c = rk != 0;
+            const double r = reg_s[p];
+            cnt += c;
+            sum += c ? r : 0.0;
+            rsum += c ? 1.0 - yb_s[p] : 0.0;
+            mx = (c && r > mx) ? r : mx;
+            top1 += c && rk == 1;
+            top5 += c && rk <= 5;
+            w5 += c && r <= 0.05;
+        }
+        if (cnt == 0) {
+            for (int i = 0; i < 8; ++i) out[i] = __builtin_nan("");
+            out[8] = 0.0;
+        } else {
+            const double p50 = 0.5 * (double)(cnt - 1), p95 = 0.95 * (double)(cnt - 1);
+            const int64_t l50 = (int64_t)__builtin_floor(p50), l95 = (int64_t)__builtin_floor(p95);
+            const int64_t h50 = l50 + 1 < cnt ? l50 + 1 : cnt - 1, h95 = l95 + 1 < cnt ? l95 + 1 : cnt - 1;
+            out[0] = sum / (double)cnt;
+            out[1] = interpolate(sorted[l50], sorted[h50], cnt, 0.5);
+            out[2] = interpolate(sorted[l95], sorted[h95], cnt, 0.95);
+            out[3] = mx;
+            out[4] = (double)top1 / (double)cnt;
+            out[5] = (double)top5 / (double)cnt;
+            out[6] = (double)w5 / (double)cnt;
+            out[7] = rsum / (double)cnt;
+            out[8] = (double)cnt;
+        }
+    }
+    for (int32_t p = threadIdx.x; p < P; p += 1024) {
+        if (regret_out) regret_out[p] = reg_s[p];
+        if (rank_out) rank_out[p] = rank_s[p];
+        if (ybar_out) ybar_out[p] = yb_s[p];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Best static configuration
 // ---------------------------------------------------------------------------
@@ -350,9 +432,14 @@ hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const
     double *stats = reinterpret_cast<double *>(w + 2 * up256((size_t)P * 8));
     int32_t *rank = reinterpret_cast<int32_t *>(w + 3 * up256((size_t)P * 8));
     hipLaunchKernelGGL(k_eval_groups, dim3(P), dim3(kEvalThreads), 0, s, rt, seg, P, idx, k, regret, rank, ybar);
-    hipLaunchKernelGGL(k_eval_select, dim3(1), dim3(kSelectThreads), 0, s, regret, rank, P, stats);
-    hipLaunchKernelGGL(k_eval_aggregate, dim3(1), dim3(256), 0, s, regret, rank, ybar, stats, P, out, regret_out,
-                       rank_out, ybar_out);
+    if (P <= kSmallP) {
+        hipLaunchKernelGGL(k_eval_small, dim3(1), dim3(1024), 0, s, regret, rank, ybar, P, out, regret_out, rank_out,
+                           ybar_out);
+    } else {
+        hipLaunchKernelGGL(k_eval_select, dim3(1), dim3(kSelectThreads), 0, s, regret, rank, P, stats);
+        hipLaunchKernelGGL(k_eval_aggregate, dim3(1), dim3(256), 0, s, regret, rank, ybar, stats, P, out, regret_out,
+                           rank_out, ybar_out);
+    }
     return hipGetLastError();
 }
 

@@ -271,6 +271,18 @@ def test_fused_selection(name):
     check_selection(w, fidx.cpu().numpy(), probs)
 
 
+@pytest.mark.parametrize("P", [4096, 4097])
+def test_evaluate_problem_count_boundary(P):
+    """Both order-statistic paths (one workgroup up to 4,096 problems, radix selection above)."""
+    say(f"evaluate {P} problems")
+    rng = np.random.default_rng(P)
+    seg = synth.ragged_segments(rng, P, 9, empty_frac=0.05)
+    R = int(seg[-1])
+    rt = rng.choice(np.array([1.0, 1.5, 2.0, 3.0, np.inf, np.nan], np.float32), R)
+    idx, _ = oracle.topk(rng.standard_normal(R).astype(np.float32), seg, 2)
+    eval_compare(rt, seg, idx)
+
+
 def test_evaluate_many_problems():
     """Order statistics over many problems (radix selection, linear in P)."""
     say("evaluate 50,000 problems")
