@@ -17,13 +17,14 @@
 //     255 when it goes right).  A pass writes the bins of every row once:
 //     128 bytes per row instead of 512.
 //   * Trees in LDS.  Trees are grouped into chunks of TC trees whose nodes
-//     (u16 code: feature | rank << 8, heap order, slot i of tree t at
-//     i*TC + t) and leaves (fp32, leaf l of tree t at l*TC + t) fill about
-//     96 KB of LDS.  Interleaving by tree puts the TC lanes of a wave that walk
-//     TC different trees on distinct banks.
-//   * Lanes.  A wave walks 64/TC rows x TC trees at a time; four such groups
-//     are in flight per wave to cover LDS latency.  For TC = 64 all lanes read
-//     the same row's bins, which lie on distinct banks (conflict-free).
+//     (u16 code: feature | rank << 8, heap order) and leaves (fp32, leaf l of
+//     tree t at l*TC + t) fill about 96 KB of LDS (128 KB for 16 trees, whose
+//     node codes are stored twice).  The node layout gives every lane of a
+//     half-wave its own LDS bank (see node_byte).
+//   * Lanes.  A wave walks 64/TC rows x TC trees at a time; several such
+//     groups are in flight per wave to cover LDS latency.  With 64 or 32
+//     trees a half-wave reads the bins of one row, whose words lie on
+//     distinct banks (conflict-free); with 16 trees it reads two rows.
 //   * Chunk-stationary, XCD-aware persistent grid.  Each workgroup owns one
 //     chunk for a whole row range and streams 256-row tiles of bins through
 //     LDS.  Workgroup b runs on XCD b % 8; the workgroups of one XCD cover the
@@ -104,14 +105,34 @@ ForestDev to_dev(const hwsel_forest_t &f)
 // ---------------------------------------------------------------------------
 constexpr int kBinSlots = 256;        // thresholds per feature incl. padding
 constexpr int kBinStrideLds = 257;    // LDS row stride (floats) of the bin table
-// Rows of bins per LDS tile: as many as fit next to a 96 KB tree chunk, in
-// whole groups per wave (more rows per wave = more walks in flight).
-__host__ __device__ constexpr int tile_rows(int tc) { return tc == 64 ? 384 : 448; }
-constexpr int kTileStride = 132;      // LDS bytes per bin row (33 dwords)
+// Rows of bins per LDS tile: as many as fit next to the tree chunk, in whole
+// groups per wave (more rows per wave = more walks in flight).  With 16
+// trees per chunk the duplicated node tables leave 32 KB: 256 rows of 128 B.
+__host__ __device__ constexpr int tile_rows(int tc) { return tc == 64 ? 384 : tc == 32 ? 448 : 256; }
+__host__ __device__ constexpr int tile_stride(int tc) { return tc == 16 ? 128 : 132; }   // LDS bytes per bin row
 constexpr int kWaves = 16;            // waves per traversal workgroup
 constexpr int kXcds = 8;
 constexpr int kSlotsPerXcd = 32;      // one workgroup per CU
 constexpr int kBinThreads = 1024;
+
+// Node codes (u16: feature | rank << 8) sit in rows of 128 bytes, one 4-byte
+// bank word per column, so that every lane of a half-wave reads its own bank
+// (a gather from 32 lanes is served in one pass only when no two lanes hit
+// one bank at different words):
+//   TC = 64: row n holds node n of every tree, tree t in column t % 32,
+//            half-word t / 32 (lanes t and t + 32 sit in different half-waves);
+//   TC = 32: tree t owns column t; node n in row n mod 2^(D-1), half-word
+//            n / 2^(D-1) (the last level uses the high half-words);
+//   TC = 16: as TC = 32 with two copies of each tree in columns t and 16 + t,
+//            one for each of the two rows that a half-wave walks.
+__host__ __device__ constexpr int node_copies(int tc) { return tc == 16 ? 2 : 1; }
+
+__host__ __device__ inline uint32_t node_byte(uint32_t n, int t, int copy, int tc, int depth)
+{
+    if (tc == 64) return n * 128u + 4u * (uint32_t)(t & 31) + 2u * (uint32_t)(t >> 5);
+    const uint32_t half = n >> (depth - 1), row = n & ((1u << (depth - 1)) - 1u);
+    return row * 128u + 4u * (uint32_t)(copy * 16 + t) + 2u * half;
+}
 
 struct PackGeom {
     int tc, n_chunks, slots, stride;      // trees per chunk, chunks, heap slots (2^D), bin row bytes
@@ -134,7 +155,7 @@ PackGeom geometry(const hwsel_forest_t &f)
     g.slots = 1 << f.depth;
     g.stride = (f.n_features + 15) / 16 * 16;
     g.thr_bytes = (size_t)f.n_features * kBinSlots * sizeof(float);
-    g.node_bytes = (size_t)g.slots * g.tc * 2;
+    g.node_bytes = (size_t)g.slots * g.tc * 2 * node_copies(g.tc);
     g.chunk_bytes = g.node_bytes + (size_t)g.slots * g.tc * 4;
     g.total = 256 + g.thr_bytes + (size_t)g.n_chunks * g.chunk_bytes;
     return g;
@@ -219,14 +240,6 @@ __device__ __forceinline__ float group_total(float v)
     return v;
 }
 
-// Position of tree t's node codes inside a heap slot.  With 64 trees a slot
-// is 128 bytes; storing tree t at 2*(t % 32) + t / 32 gives the 32 lanes of
-// each half-wave 32 distinct banks.
-__host__ __device__ __forceinline__ int node_pos(int t, int tc)
-{
-    return tc == 64 ? 2 * (t & 31) + (t >> 5) : t;
-}
-
 template <int TC, int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__restrict__ chunks, int n_chunks,
                                                               const uint8_t *__restrict__ Xb, int64_t R,
@@ -234,24 +247,31 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
                                                               int64_t rows_per_group, float *__restrict__ partial)
 {
     constexpr int NS = 1 << D;
-    constexpr int NODE_B = NS * TC * 2;
-    constexpr int CHUNK_B = NS * TC * 6;
+    constexpr int NODE_B = NS * TC * 2 * node_copies(TC);
+    constexpr int CHUNK_B = NODE_B + NS * TC * 4;
     constexpr int RPI = 64 / TC;                       // rows per lane group
     constexpr int kTileRows = tile_rows(TC);
-    constexpr int ROWS_PER_WAVE = kTileRows / kWaves;  // 24 or 28
+    constexpr int kStride = tile_stride(TC);
+    // With 16 trees the group totals go straight to the partial rows: the
+    // chunk and the bin tile fill the whole LDS.
+    constexpr bool kDirect = TC == 16;
+    constexpr int ROWS_PER_WAVE = kTileRows / kWaves;
     constexpr int GROUPS = ROWS_PER_WAVE / RPI;
     constexpr int ILP = GROUPS % 8 == 0 ? 8 : GROUPS % 7 == 0 ? 7 : GROUPS % 6 == 0 ? 6 : 4;   // groups in flight
     constexpr int ITER = ROWS_PER_WAVE / (RPI * ILP);
     static_assert(ITER >= 1 && ITER * RPI * ILP == ROWS_PER_WAVE, "tile shape");
-    __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kTileStride + kTileRows * 4];
-    const uint16_t *nodes = reinterpret_cast<const uint16_t *>(lds);
+    static_assert(CHUNK_B + kTileRows * kStride + (kDirect ? 0 : kTileRows * 4) <= 160 * 1024, "LDS");
+    __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kStride + (kDirect ? 0 : kTileRows * 4)];
     const float *leaves = reinterpret_cast<const float *>(lds + NODE_B);
     uint8_t *bins = lds + CHUNK_B;
-    float *rowsum = reinterpret_cast<float *>(lds + CHUNK_B + kTileRows * kTileStride);
+    float *rowsum = reinterpret_cast<float *>(lds + CHUNK_B + kTileRows * kStride);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int t = lane % TC, s = lane / TC;
-    const int npos = node_pos(t, TC);
+    // Byte offset of node n is (n << 7) + k_lo, or (n << 7) + k_hi on the
+    // last level of a TC < 64 layout (high half-words, rows from 0 again).
+    const uint32_t k_lo = node_byte(0, t, node_copies(TC) == 2 ? (s & 1) : 0, TC, D);
+    const uint32_t k_hi = k_lo + 2u - (TC < 64 ? (1u << (D + 6)) : 2u);
     const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
     const int slots = gridDim.x / kXcds;
     const int items = n_chunks * groups_per_xcd;
@@ -292,8 +312,12 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
                 const int e = threadIdx.x + q * 64 * kWaves;
                 const int rr = e / vpr, w = e - rr * vpr;
                 if (rr < kTileRows) {
-                    uint32_t *d = reinterpret_cast<uint32_t *>(bins + rr * kTileStride + 16 * w);
-                    d[0] = pre[q].x; d[1] = pre[q].y; d[2] = pre[q].z; d[3] = pre[q].w;
+                    if constexpr (kStride % 16 == 0) {
+                        *reinterpret_cast<uint4 *>(bins + rr * kStride + 16 * w) = pre[q];
+                    } else {
+                        uint32_t *d = reinterpret_cast<uint32_t *>(bins + rr * kStride + 16 * w);
+                        d[0] = pre[q].x; d[1] = pre[q].y; d[2] = pre[q].z; d[3] = pre[q].w;
+                    }
                 }
             }
             __syncthreads();
@@ -305,25 +329,34 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
 #pragma unroll
                 for (int a = 0; a < ILP; ++a) {
                     const int row = wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s;
-                    rowp[a] = bins + row * kTileStride;
+                    rowp[a] = bins + row * kStride;
                     node[a] = 1;
                 }
 #pragma unroll
                 for (int l = 0; l < D; ++l) {
                     uint32_t code[ILP];
+                    const uint32_t k = l == D - 1 ? k_hi : k_lo;
 #pragma unroll
-                    for (int a = 0; a < ILP; ++a) code[a] = nodes[node[a] * TC + npos];
+                    for (int a = 0; a < ILP; ++a)
+                        code[a] = *reinterpret_cast<const uint16_t *>(lds + ((uint32_t)node[a] << 7) + k);
 #pragma unroll
                     for (int a = 0; a < ILP; ++a) node[a] = descend(node[a], code[a], rowp[a][code[a] & 0xffu]);
                 }
 #pragma unroll
                 for (int a = 0; a < ILP; ++a) {
                     const float v = group_total<TC>(leaves[(node[a] - NS) * TC + t]);
-                    if (t == TC - 1) rowsum[wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s] = v;
+                    const int row = wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s;
+                    if constexpr (kDirect) {
+                        if (t == TC - 1 && row < n_tile) partial[(int64_t)c * R + t0 + row] = v;
+                    } else if (t == TC - 1) {
+                        rowsum[row] = v;
+                    }
                 }
             }
-            __syncthreads();
-            for (int e = threadIdx.x; e < n_tile; e += 64 * kWaves) partial[(int64_t)c * R + t0 + e] = rowsum[e];
+            if constexpr (!kDirect) {
+                __syncthreads();
+                for (int e = threadIdx.x; e < n_tile; e += 64 * kWaves) partial[(int64_t)c * R + t0 + e] = rowsum[e];
+            }
         }
     }
 }
@@ -452,7 +485,7 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
     }
     uint8_t *chunk0 = img.data() + 256 + g.thr_bytes;
     for (int c = 0; c < g.n_chunks; ++c) {
-        uint16_t *nodes = reinterpret_cast<uint16_t *>(chunk0 + (size_t)c * g.chunk_bytes);
+        uint8_t *nodes = chunk0 + (size_t)c * g.chunk_bytes;
         float *leaves = reinterpret_cast<float *>(chunk0 + (size_t)c * g.chunk_bytes + g.node_bytes);
         for (int tt = 0; tt < g.tc; ++tt) {
             const int64_t tree = (int64_t)c * g.tc + tt;
@@ -463,14 +496,16 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
                 v = v == 0.0f ? 0.0f : v;
                 const auto &u = U[fj];
                 const int rank = (int)(std::lower_bound(u.begin(), u.end(), v) - u.begin());
-                nodes[(n + 1) * g.tc + node_pos(tt, g.tc)] = (uint16_t)(fj | (rank << 8));
+                const uint16_t code = (uint16_t)(fj | (rank << 8));
+                for (int copy = 0; copy < node_copies(g.tc); ++copy)
+                    std::memcpy(nodes + node_byte((uint32_t)(n + 1), tt, copy, g.tc, f.depth), &code, 2);
             }
             for (int64_t l = 0; l <= n_int; ++l) leaves[l * g.tc + tt] = leaf[tree * (n_int + 1) + l];
         }
     }
     int32_t *hdr = reinterpret_cast<int32_t *>(img.data());
     hdr[0] = 0x48575346;   // "FSWH"
-    hdr[1] = 1;
+    hdr[1] = 2;
     hdr[2] = f.n_trees; hdr[3] = f.depth; hdr[4] = f.n_features; hdr[5] = g.tc; hdr[6] = g.n_chunks;
     if (hipMemcpyAsync(packed, img.data(), g.total, hipMemcpyHostToDevice, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
