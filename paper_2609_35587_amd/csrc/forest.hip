@@ -115,23 +115,24 @@ constexpr int kXcds = 8;
 constexpr int kSlotsPerXcd = 32;      // one workgroup per CU
 constexpr int kBinThreads = 1024;
 
-// Node codes (u16: feature | rank << 8) sit in rows of 128 bytes, one 4-byte
-// bank word per column, so that every lane of a half-wave reads its own bank
-// (a gather from 32 lanes is served in one pass only when no two lanes hit
-// one bank at different words):
-//   TC = 64: row n holds node n of every tree, tree t in column t % 32,
-//            half-word t / 32 (lanes t and t + 32 sit in different half-waves);
-//   TC = 32: tree t owns column t; node n in row n mod 2^(D-1), half-word
-//            n / 2^(D-1) (the last level uses the high half-words);
-//   TC = 16: as TC = 32 with two copies of each tree in columns t and 16 + t,
-//            one for each of the two rows that a half-wave walks.
+// Node codes (u16: feature | rank << 8) are stored as sibling pairs: the
+// 4-byte word of pair p holds nodes 2p (low half) and 2p + 1 (high half), so
+// one read fetches both children of node p (pair 0 holds the root in its high
+// half).  Pair p of every tree sits in row p; each tree owns one 4-byte column
+// (one LDS bank), so every lane of a half-wave reads its own bank (a gather
+// from 32 lanes is served in one pass only when no two lanes hit one bank at
+// different words):
+//   TC = 64: rows of 256 bytes, tree t in column t (lanes t and t + 32 sit
+//            in different half-waves);
+//   TC = 32: rows of 128 bytes, tree t in column t;
+//   TC = 16: rows of 128 bytes holding two copies of every tree, in columns
+//            t and 16 + t, one for each of the two rows a half-wave walks.
 __host__ __device__ constexpr int node_copies(int tc) { return tc == 16 ? 2 : 1; }
+__host__ __device__ constexpr uint32_t pair_row_bytes(int tc) { return tc == 64 ? 256u : 128u; }
 
-__host__ __device__ inline uint32_t node_byte(uint32_t n, int t, int copy, int tc, int depth)
+__host__ __device__ inline uint32_t node_byte(uint32_t n, int t, int copy, int tc)
 {
-    if (tc == 64) return n * 128u + 4u * (uint32_t)(t & 31) + 2u * (uint32_t)(t >> 5);
-    const uint32_t half = n >> (depth - 1), row = n & ((1u << (depth - 1)) - 1u);
-    return row * 128u + 4u * (uint32_t)(copy * 16 + t) + 2u * half;
+    return (n >> 1) * pair_row_bytes(tc) + 4u * (uint32_t)(copy * 16 + t) + 2u * (n & 1u);
 }
 
 struct PackGeom {
@@ -218,6 +219,22 @@ __device__ __forceinline__ int descend(int node, uint32_t code, uint32_t bin)
     return out;
 }
 
+// descend() that also takes the child's code from the children pair (low
+// half for the left child, high half for the right one) with the same carry.
+__device__ __forceinline__ void descend_pair(int &node, uint32_t &code, uint32_t bin, uint32_t pair)
+{
+    int n_out;
+    uint32_t c_out, scratch;
+    asm("v_sub_co_u32_sdwa %2, vcc, %3, %4 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD\n\t"
+        "v_cndmask_b32_sdwa %1, %5, %5, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t"
+        "v_addc_co_u32_e32 %0, vcc, %6, %6, vcc"
+        : "=&v"(n_out), "=&v"(c_out), "=&v"(scratch)
+        : "v"(code), "v"(bin), "v"(pair), "v"(node)
+        : "vcc");
+    node = n_out;
+    code = c_out;
+}
+
 template <int CTRL, int ROW_MASK, bool ZERO_FILL>
 __device__ __forceinline__ float dpp_add(float v)
 {
@@ -268,10 +285,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int t = lane % TC, s = lane / TC;
-    // Byte offset of node n is (n << 7) + k_lo, or (n << 7) + k_hi on the
-    // last level of a TC < 64 layout (high half-words, rows from 0 again).
-    const uint32_t k_lo = node_byte(0, t, node_copies(TC) == 2 ? (s & 1) : 0, TC, D);
-    const uint32_t k_hi = k_lo + 2u - (TC < 64 ? (1u << (D + 6)) : 2u);
+    // The children pair of node n is the word at n * ROW_B + col.
+    constexpr uint32_t ROW_B = pair_row_bytes(TC);
+    const uint32_t col = node_byte(0, t, node_copies(TC) == 2 ? (s & 1) : 0, TC);
     const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
     const int slots = gridDim.x / kXcds;
     const int items = n_chunks * groups_per_xcd;
@@ -325,22 +341,32 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
 #pragma unroll 1
             for (int it = 0; it < ITER; ++it) {
                 int node[ILP];
+                uint32_t code[ILP];
                 const uint8_t *rowp[ILP];
 #pragma unroll
                 for (int a = 0; a < ILP; ++a) {
                     const int row = wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s;
                     rowp[a] = bins + row * kStride;
                     node[a] = 1;
+                    code[a] = *reinterpret_cast<const uint16_t *>(lds + col + 2);   // root: high half of pair 0
                 }
+                // Per level: the bin of the current node and the pair of its
+                // children are read together; the compare then picks the
+                // child's code from the pair, so a level waits for one LDS
+                // round trip.
 #pragma unroll
                 for (int l = 0; l < D; ++l) {
-                    uint32_t code[ILP];
-                    const uint32_t k = l == D - 1 ? k_hi : k_lo;
+                    uint32_t bin[ILP], pair[ILP];
 #pragma unroll
-                    for (int a = 0; a < ILP; ++a)
-                        code[a] = *reinterpret_cast<const uint16_t *>(lds + ((uint32_t)node[a] << 7) + k);
+                    for (int a = 0; a < ILP; ++a) {
+                        bin[a] = rowp[a][code[a] & 0xffu];
+                        if (l < D - 1) pair[a] = *reinterpret_cast<const uint32_t *>(lds + (uint32_t)node[a] * ROW_B + col);
+                    }
 #pragma unroll
-                    for (int a = 0; a < ILP; ++a) node[a] = descend(node[a], code[a], rowp[a][code[a] & 0xffu]);
+                    for (int a = 0; a < ILP; ++a) {
+                        if (l < D - 1) descend_pair(node[a], code[a], bin[a], pair[a]);
+                        else node[a] = descend(node[a], code[a], bin[a]);
+                    }
                 }
 #pragma unroll
                 for (int a = 0; a < ILP; ++a) {
@@ -498,7 +524,7 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
                 const int rank = (int)(std::lower_bound(u.begin(), u.end(), v) - u.begin());
                 const uint16_t code = (uint16_t)(fj | (rank << 8));
                 for (int copy = 0; copy < node_copies(g.tc); ++copy)
-                    std::memcpy(nodes + node_byte((uint32_t)(n + 1), tt, copy, g.tc, f.depth), &code, 2);
+                    std::memcpy(nodes + node_byte((uint32_t)(n + 1), tt, copy, g.tc), &code, 2);
             }
             for (int64_t l = 0; l <= n_int; ++l) leaves[l * g.tc + tt] = leaf[tree * (n_int + 1) + l];
         }
