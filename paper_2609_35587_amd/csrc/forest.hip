@@ -269,19 +269,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
     constexpr int RPI = 64 / TC;                       // rows per lane group
     constexpr int kTileRows = tile_rows(TC);
     constexpr int kStride = tile_stride(TC);
-    // With 16 trees the group totals go straight to the partial rows: the
-    // chunk and the bin tile fill the whole LDS.
-    constexpr bool kDirect = TC == 16;
     constexpr int ROWS_PER_WAVE = kTileRows / kWaves;
     constexpr int GROUPS = ROWS_PER_WAVE / RPI;
     constexpr int ILP = GROUPS % 8 == 0 ? 8 : GROUPS % 7 == 0 ? 7 : GROUPS % 6 == 0 ? 6 : 4;   // groups in flight
     constexpr int ITER = ROWS_PER_WAVE / (RPI * ILP);
     static_assert(ITER >= 1 && ITER * RPI * ILP == ROWS_PER_WAVE, "tile shape");
-    static_assert(CHUNK_B + kTileRows * kStride + (kDirect ? 0 : kTileRows * 4) <= 160 * 1024, "LDS");
-    __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kStride + (kDirect ? 0 : kTileRows * 4)];
+    static_assert(CHUNK_B + kTileRows * kStride <= 160 * 1024, "LDS");
+    __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kStride];
     const float *leaves = reinterpret_cast<const float *>(lds + NODE_B);
-    uint8_t *bins = lds + CHUNK_B;
-    float *rowsum = reinterpret_cast<float *>(lds + CHUNK_B + kTileRows * kStride);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int t = lane % TC, s = lane / TC;
@@ -291,6 +286,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
     const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
     const int slots = gridDim.x / kXcds;
     const int items = n_chunks * groups_per_xcd;
+    // Each wave owns ROWS_PER_WAVE rows of every tile and a private LDS region
+    // for their bins, which it refills on its own (no workgroup barrier
+    // between tiles): its next rows are fetched into registers while it walks
+    // the current ones.
+    uint8_t *region = lds + CHUNK_B + wave * ROWS_PER_WAVE * kStride;
+    constexpr int kVec = (ROWS_PER_WAVE * 8 + 63) / 64;   // uint4 per lane for 128-byte rows
+    const int vpr = stride >> 4;                         // uint4 per bin row
 
     for (int item = slot; item < items; item += slots) {
         const int c = item % n_chunks, sub = item / n_chunks;
@@ -303,41 +305,41 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
             uint4 *dst = reinterpret_cast<uint4 *>(lds);
             for (int e = threadIdx.x; e < CHUNK_B / 16; e += 64 * kWaves) dst[e] = src[e];
         }
-        // Bin tiles stream through registers: tile k+1 is fetched from global
-        // memory while tile k is walked from LDS.
-        constexpr int kVec = (kTileRows * 128 / 16 + 64 * kWaves - 1) / (64 * kWaves);   // uint4 per thread
-        const int vpr = stride >> 4;                                  // uint4 per bin row
+        __syncthreads();
+        const uint32_t root = *reinterpret_cast<const uint16_t *>(lds + col + 2);   // high half of pair 0
         uint4 pre[kVec];
         auto fetch = [&](int64_t t0) {
-            const int n = (int)(r_end - t0 < kTileRows ? r_end - t0 : kTileRows);
+            const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
+            const int64_t n = r_end - w0;                  // rows of this wave left (may be <= 0)
 #pragma unroll
             for (int q = 0; q < kVec; ++q) {
-                const int e = threadIdx.x + q * 64 * kWaves;
+                const int e = lane + 64 * q;
                 const int rr = e / vpr, w = e - rr * vpr;
-                pre[q] = (rr < n && t0 < r_end)
-                             ? reinterpret_cast<const uint4 *>(Xb + (t0 + rr) * stride)[w]
-                             : make_uint4(0, 0, 0, 0);
+                pre[q] = (rr < ROWS_PER_WAVE && rr < n) ? reinterpret_cast<const uint4 *>(Xb + (w0 + rr) * stride)[w]
+                                                        : make_uint4(0, 0, 0, 0);
             }
         };
         fetch(r_begin);
         for (int64_t t0 = r_begin; t0 < r_end; t0 += kTileRows) {
-            const int n_tile = (int)(r_end - t0 < kTileRows ? r_end - t0 : kTileRows);
-            __syncthreads();
+            const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
+            // The previous rows' reads have all returned (their results were
+            // used), so the region can be overwritten.
 #pragma unroll
             for (int q = 0; q < kVec; ++q) {
-                const int e = threadIdx.x + q * 64 * kWaves;
+                const int e = lane + 64 * q;
                 const int rr = e / vpr, w = e - rr * vpr;
-                if (rr < kTileRows) {
+                if (rr < ROWS_PER_WAVE) {
                     if constexpr (kStride % 16 == 0) {
-                        *reinterpret_cast<uint4 *>(bins + rr * kStride + 16 * w) = pre[q];
+                        *reinterpret_cast<uint4 *>(region + rr * kStride + 16 * w) = pre[q];
                     } else {
-                        uint32_t *d = reinterpret_cast<uint32_t *>(bins + rr * kStride + 16 * w);
+                        uint32_t *d = reinterpret_cast<uint32_t *>(region + rr * kStride + 16 * w);
                         d[0] = pre[q].x; d[1] = pre[q].y; d[2] = pre[q].z; d[3] = pre[q].w;
                     }
                 }
             }
-            __syncthreads();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the region is written before any lane reads it
             fetch(t0 + kTileRows);
+            if (w0 >= r_end) continue;                               // wave-uniform: no rows left here
 #pragma unroll 1
             for (int it = 0; it < ITER; ++it) {
                 int node[ILP];
@@ -345,10 +347,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
                 const uint8_t *rowp[ILP];
 #pragma unroll
                 for (int a = 0; a < ILP; ++a) {
-                    const int row = wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s;
-                    rowp[a] = bins + row * kStride;
+                    rowp[a] = region + ((it * ILP + a) * RPI + s) * kStride;
                     node[a] = 1;
-                    code[a] = *reinterpret_cast<const uint16_t *>(lds + col + 2);   // root: high half of pair 0
+                    code[a] = root;
                 }
                 // Per level: the bin of the current node and the pair of its
                 // children are read together; the compare then picks the
@@ -371,17 +372,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
 #pragma unroll
                 for (int a = 0; a < ILP; ++a) {
                     const float v = group_total<TC>(leaves[(node[a] - NS) * TC + t]);
-                    const int row = wave * ROWS_PER_WAVE + (it * ILP + a) * RPI + s;
-                    if constexpr (kDirect) {
-                        if (t == TC - 1 && row < n_tile) partial[(int64_t)c * R + t0 + row] = v;
-                    } else if (t == TC - 1) {
-                        rowsum[row] = v;
-                    }
+                    const int64_t row = w0 + (it * ILP + a) * RPI + s;
+                    if (t == TC - 1 && row < r_end) partial[(int64_t)c * R + row] = v;
                 }
-            }
-            if constexpr (!kDirect) {
-                __syncthreads();
-                for (int e = threadIdx.x; e < n_tile; e += 64 * kWaves) partial[(int64_t)c * R + t0 + e] = rowsum[e];
             }
         }
     }
