@@ -235,26 +235,56 @@ __device__ __forceinline__ void descend_pair(int &node, uint32_t &code, uint32_t
     code = c_out;
 }
 
+// The root's step: as descend_pair, and with the same carry also picks the
+// children pair of the chosen child (p2 for node 2, p3 for node 3).
+__device__ __forceinline__ void descend_root(int &node, uint32_t &code, uint32_t &pair, uint32_t bin, uint32_t p1,
+                                             uint32_t p2, uint32_t p3)
+{
+    int n_out;
+    uint32_t c_out, p_out, scratch;
+    asm("v_sub_co_u32_sdwa %3, vcc, %4, %5 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD\n\t"
+        "v_cndmask_b32_sdwa %1, %6, %6, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t"
+        "v_cndmask_b32_e32 %2, %7, %8, vcc\n\t"
+        "v_addc_co_u32_e32 %0, vcc, %9, %9, vcc"
+        : "=&v"(n_out), "=&v"(c_out), "=&v"(p_out), "=&v"(scratch)
+        : "v"(code), "v"(bin), "v"(p1), "v"(p2), "v"(p3), "v"(node)
+        : "vcc");
+    node = n_out;
+    code = c_out;
+    pair = p_out;
+}
+
 template <int CTRL, int ROW_MASK, bool ZERO_FILL>
 __device__ __forceinline__ float dpp_add(float v)
 {
     return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xf, ZERO_FILL));
 }
 
-// Sum over each aligned group of TC lanes (TC in {16, 32, 64}) with DPP:
-// an inclusive scan inside 16-lane rows, then row broadcasts.  The last lane
-// of each group ends with the group's total, always in the same order.
-template <int TC>
-__device__ __forceinline__ float group_total(float v)
+// Sums over each aligned group of TC lanes (TC in {16, 32, 64}) of N
+// independent values with DPP: an inclusive scan inside 16-lane rows, then
+// row broadcasts.  The last lane of each group ends with the group's total,
+// always in the same order.  The values advance stage by stage so that the
+// dependent DPP steps of one are interleaved with the others'.
+template <int TC, int N>
+__device__ __forceinline__ void group_totals(float (&v)[N])
 {
     static_assert(TC == 16 || TC == 32 || TC == 64, "group width");
-    v = dpp_add<0x111, 0xf, true>(v);   // row_shr:1
-    v = dpp_add<0x112, 0xf, true>(v);   // row_shr:2
-    v = dpp_add<0x114, 0xf, true>(v);   // row_shr:4
-    v = dpp_add<0x118, 0xf, true>(v);   // row_shr:8
-    if constexpr (TC >= 32) v = dpp_add<0x142, 0xa, false>(v);   // row_bcast:15 into rows 1, 3
-    if constexpr (TC >= 64) v = dpp_add<0x143, 0xc, false>(v);   // row_bcast:31 into rows 2, 3
-    return v;
+#pragma unroll
+    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x111, 0xf, true>(v[a]);
+#pragma unroll
+    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x112, 0xf, true>(v[a]);
+#pragma unroll
+    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x114, 0xf, true>(v[a]);
+#pragma unroll
+    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x118, 0xf, true>(v[a]);
+    if constexpr (TC >= 32) {
+#pragma unroll
+        for (int a = 0; a < N; ++a) v[a] = dpp_add<0x142, 0xa, false>(v[a]);
+    }
+    if constexpr (TC >= 64) {
+#pragma unroll
+        for (int a = 0; a < N; ++a) v[a] = dpp_add<0x143, 0xc, false>(v[a]);
+    }
 }
 
 template <int TC, int D>
@@ -306,7 +336,12 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
             for (int e = threadIdx.x; e < CHUNK_B / 16; e += 64 * kWaves) dst[e] = src[e];
         }
         __syncthreads();
+        // The root's code and the children pairs of nodes 1, 2, 3 are the same
+        // for every row: registers for the whole chunk.
         const uint32_t root = *reinterpret_cast<const uint16_t *>(lds + col + 2);   // high half of pair 0
+        const uint32_t p1 = D >= 2 ? *reinterpret_cast<const uint32_t *>(lds + ROW_B + col) : 0u;
+        const uint32_t p2 = D >= 3 ? *reinterpret_cast<const uint32_t *>(lds + 2 * ROW_B + col) : 0u;
+        const uint32_t p3 = D >= 3 ? *reinterpret_cast<const uint32_t *>(lds + 3 * ROW_B + col) : 0u;
         uint4 pre[kVec];
         auto fetch = [&](int64_t t0) {
             const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
@@ -354,26 +389,41 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
                 // Per level: the bin of the current node and the pair of its
                 // children are read together; the compare then picks the
                 // child's code from the pair, so a level waits for one LDS
-                // round trip.
+                // round trip.  Levels 0 and 1 take their pairs from registers.
+                uint32_t pair[ILP];
 #pragma unroll
                 for (int l = 0; l < D; ++l) {
-                    uint32_t bin[ILP], pair[ILP];
+                    uint32_t bin[ILP];
 #pragma unroll
                     for (int a = 0; a < ILP; ++a) {
                         bin[a] = rowp[a][code[a] & 0xffu];
-                        if (l < D - 1) pair[a] = *reinterpret_cast<const uint32_t *>(lds + (uint32_t)node[a] * ROW_B + col);
+                        if (l >= 2 && l < D - 1)
+                            pair[a] = *reinterpret_cast<const uint32_t *>(lds + (uint32_t)node[a] * ROW_B + col);
                     }
 #pragma unroll
                     for (int a = 0; a < ILP; ++a) {
-                        if (l < D - 1) descend_pair(node[a], code[a], bin[a], pair[a]);
-                        else node[a] = descend(node[a], code[a], bin[a]);
+                        if (l == D - 1) node[a] = descend(node[a], code[a], bin[a]);
+                        else if (l == 0 && D >= 3) descend_root(node[a], code[a], pair[a], bin[a], p1, p2, p3);
+                        else if (l == 0) descend_pair(node[a], code[a], bin[a], p1);
+                        else descend_pair(node[a], code[a], bin[a], pair[a]);
                     }
                 }
+                // Leaves of all groups first, then the sums, then the stores
+                // (one lane per row), so that nothing serialises the groups.
+                float v[ILP];
 #pragma unroll
-                for (int a = 0; a < ILP; ++a) {
-                    const float v = group_total<TC>(leaves[(node[a] - NS) * TC + t]);
-                    const int64_t row = w0 + (it * ILP + a) * RPI + s;
-                    if (t == TC - 1 && row < r_end) partial[(int64_t)c * R + row] = v;
+                for (int a = 0; a < ILP; ++a) v[a] = leaves[(node[a] - NS) * TC + t];
+                group_totals<TC, ILP>(v);
+                float *out = partial + (int64_t)c * R + w0 + it * ILP * RPI + s;
+                if (w0 + ROWS_PER_WAVE <= r_end) {                   // wave-uniform: every row is real
+                    if (t == TC - 1) {
+#pragma unroll
+                        for (int a = 0; a < ILP; ++a) out[a * RPI] = v[a];
+                    }
+                } else if (t == TC - 1) {
+#pragma unroll
+                    for (int a = 0; a < ILP; ++a)
+                        if (w0 + (it * ILP + a) * RPI + s < r_end) out[a * RPI] = v[a];
                 }
             }
         }
