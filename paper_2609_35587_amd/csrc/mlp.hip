@@ -75,7 +75,11 @@ __device__ __forceinline__ float gelu_as(float a)
     q *= q;
     q *= q;
     q *= q;
-    return fmaf(-x, __builtin_amdgcn_rcpf(q), fmaxf(a, 0.0f));
+    // max(a, 0) without the NaN-quieting copy the compiler adds to fmaxf
+    // (a is a finite accumulator here)
+    float pos;
+    asm("v_max_f32_e32 %0, 0, %1" : "=v"(pos) : "v"(a));
+    return fmaf(-x, __builtin_amdgcn_rcpf(q), pos);
 }
 
 // ---------------------------------------------------------------------------
