@@ -104,7 +104,10 @@ ForestDev to_dev(const hwsel_forest_t &f)
 // Packed path: layout
 // ---------------------------------------------------------------------------
 constexpr int kBinSlots = 256;        // thresholds per feature incl. padding
-constexpr int kBinStrideLds = 257;    // LDS row stride (floats) of the bin table
+// Bin table in LDS: threshold i of feature f at word
+// (f / 32) * 32 * kBinSlots + 32 * i + f % 32, so the 32 features searched by
+// a half-wave each stay on their own bank whatever their search positions.
+__host__ __device__ constexpr int bin_table_index(int f, int i) { return (f >> 5) * 32 * kBinSlots + 32 * i + (f & 31); }
 // Rows of bins per LDS tile: as many as fit next to the tree chunk, in whole
 // groups per wave (more rows per wave = more walks in flight).  With 16
 // trees per chunk the duplicated node tables leave 32 KB: 256 rows of 128 B.
@@ -171,14 +174,13 @@ __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict_
                                                          const float *__restrict__ U, int nf, uint32_t nan_bin,
                                                          uint8_t *__restrict__ Xb, int stride)
 {
-    __shared__ float u[128 * kBinStrideLds];
-    for (int e = threadIdx.x; e < nf * kBinSlots; e += kBinThreads)
-        u[(e >> 8) * kBinStrideLds + (e & 255)] = U[e];
+    __shared__ float u[128 * kBinSlots];
+    for (int e = threadIdx.x; e < nf * kBinSlots; e += kBinThreads) u[bin_table_index(e >> 8, e & 255)] = U[e];
     __syncthreads();
     const int f = threadIdx.x & 127;
     const int sub = threadIdx.x >> 7;                 // 8 row lanes per block
     if (f >= stride) return;
-    const float *uf = u + f * kBinStrideLds;
+    const float *uf = u + bin_table_index(f, 0);
     constexpr int kRowsPerThread = 8;                 // independent searches in flight
     const int64_t step_rows = (int64_t)gridDim.x * 8 * kRowsPerThread;
     for (int64_t r0 = ((int64_t)blockIdx.x * 8 + sub) * kRowsPerThread; r0 < R; r0 += step_rows) {
@@ -192,7 +194,7 @@ __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict_
 #pragma unroll
         for (int step = 128; step > 0; step >>= 1) {
 #pragma unroll
-            for (int q = 0; q < kRowsPerThread; ++q) bin[q] += (uf[bin[q] + step - 1] <= x[q]) ? step : 0;
+            for (int q = 0; q < kRowsPerThread; ++q) bin[q] += (uf[32 * (bin[q] + step - 1)] <= x[q]) ? step : 0;
         }
 #pragma unroll
         for (int q = 0; q < kRowsPerThread; ++q) {
