@@ -17,21 +17,26 @@
 //     255 when it goes right).  A pass writes the bins of every row once:
 //     128 bytes per row instead of 512.
 //   * Trees in LDS.  Trees are grouped into chunks of TC trees whose nodes
-//     (u16 code: feature | rank << 8, heap order) and leaves (fp32, leaf l of
-//     tree t at l*TC + t) fill about 96 KB of LDS (128 KB for 16 trees, whose
-//     node codes are stored twice).  The node layout gives every lane of a
-//     half-wave its own LDS bank (see node_byte).
+//     (u16 code: feature | rank << 8, heap order, stored as sibling pairs so
+//     one 4-byte read fetches both children of a node) and leaves (fp32,
+//     leaf l of tree t at l*TC + t) fill about 96 KB of LDS (128 KB for 16
+//     trees, whose node pairs are stored twice).  The node layout gives every
+//     lane of a half-wave its own LDS bank (see node_byte).
 //   * Lanes.  A wave walks 64/TC rows x TC trees at a time; several such
-//     groups are in flight per wave to cover LDS latency.  With 64 or 32
-//     trees a half-wave reads the bins of one row, whose words lie on
-//     distinct banks (conflict-free); with 16 trees it reads two rows.
+//     groups are in flight per wave to cover LDS latency.  A level reads the
+//     bin of the current node and the children pair together, then picks the
+//     child's code with the compare's carry: one LDS round trip per level.
+//     With 64 or 32 trees a half-wave reads the bins of one row, whose words
+//     lie on distinct banks (conflict-free); with 16 trees it reads two rows.
 //   * Chunk-stationary, XCD-aware persistent grid.  Each workgroup owns one
-//     chunk for a whole row range and streams 256-row tiles of bins through
-//     LDS.  Workgroup b runs on XCD b % 8; the workgroups of one XCD cover the
-//     same rows with different chunks, in step, so a tile is fetched from HBM
-//     once per XCD and re-read from that XCD's L2.
-//   * Deterministic sums.  A chunk's per-row sum is a fixed butterfly over
-//     its TC lanes, written to a per-chunk partial row; a last pass adds
+//     chunk for a whole row range; each wave owns a slice of every row tile
+//     and a private LDS region for its bins, refilled without workgroup
+//     barriers while the next slice is fetched into registers.  Workgroup b
+//     runs on XCD b % 8; the workgroups of one XCD cover the same rows with
+//     different chunks, so a tile is fetched from HBM about once per XCD and
+//     re-read from that XCD's L2.
+//   * Deterministic sums.  A chunk's per-row sum is a fixed DPP reduction
+//     over its TC lanes, written to a per-chunk partial row; a last pass adds
 //     base + partials in chunk order.
 #include <algorithm>
 #include <cstring>
