@@ -219,6 +219,15 @@ def test_mlp_dataset_rows():
     say("mlp: fp32 row-block path on the sample")
     g2 = hwsel.hwsel_mlp_score(d.mlp, X.index_select(0, rows_d).contiguous()).cpu().numpy()
     say("  max err/bound %.3g  rms %.3g" % _assert_mlp(g2, o))
+    # every row: the matrix-core path against the independent fp32 row-block
+    # path (itself checked against the oracle above), so that a wrong tile
+    # anywhere in the 4.9 M rows is caught, not only in the sample
+    say("mlp: matrix-core vs fp32 row-block path on all rows")
+    s_ref = hwsel.hwsel_mlp_score(d.mlp, X).double()
+    rms = float(torch.sqrt(torch.mean(s_ref ** 2)))
+    ratio = torch.abs(s.double() - s_ref) / (2e-2 * torch.clamp(torch.abs(s_ref), min=rms))
+    say("  max |diff| / (2e-2 max(|ref|, rms)) %.3g" % float(ratio.max()))
+    assert float(ratio.max()) <= 1.0
     # top-k on the MLP scores: admissible picks (oracle score within the tie band of the k-th)
     idx, _ = hwsel.hwsel_topk_per_problem(s, d.seg, w.cfg.k)
     idx = idx.cpu().numpy()
