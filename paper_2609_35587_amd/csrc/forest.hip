@@ -179,35 +179,45 @@ __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict_
                                                          const float *__restrict__ U, int nf, uint32_t nan_bin,
                                                          uint8_t *__restrict__ Xb, int stride)
 {
-    __shared__ float u[128 * kBinSlots];
-    for (int e = threadIdx.x; e < nf * kBinSlots; e += kBinThreads) u[bin_table_index(e >> 8, e & 255)] = U[e];
+    // thresholds as order-preserving keys; index i of feature f at
+    // bin_table_index(f, i), so each searched feature stays on its own bank
+    __shared__ uint32_t u[128 * kBinSlots];
+    for (int e = threadIdx.x; e < nf * kBinSlots; e += kBinThreads)
+        u[bin_table_index(e >> 8, e & 255)] = order_key(U[e]);
     __syncthreads();
     const int f = threadIdx.x & 127;
     const int sub = threadIdx.x >> 7;                 // 8 row lanes per block
     if (f >= stride) return;
-    const float *uf = u + bin_table_index(f, 0);
+    const uint8_t *uf = reinterpret_cast<const uint8_t *>(u + bin_table_index(f, 0));
     constexpr int kRowsPerThread = 8;                 // independent searches in flight
     const int64_t step_rows = (int64_t)gridDim.x * 8 * kRowsPerThread;
     for (int64_t r0 = ((int64_t)blockIdx.x * 8 + sub) * kRowsPerThread; r0 < R; r0 += step_rows) {
         float x[kRowsPerThread];
-        uint32_t bin[kRowsPerThread];
+        uint32_t kx1[kRowsPerThread], b[kRowsPerThread];
 #pragma unroll
         for (int q = 0; q < kRowsPerThread; ++q) {
             x[q] = (f < nf && r0 + q < R) ? X[(r0 + q) * ld + f] : 0.0f;
-            bin[q] = 0;
+            kx1[q] = order_key(x[q] == 0.0f ? 0.0f : x[q]) + 1u;
+            b[q] = 0;
         }
+        // b = #{u <= x} built from the top bit: at step k the probe is
+        // threshold (b << (k + 1)) + 2^k - 1 (rows of 32 words, 128 bytes)
 #pragma unroll
-        for (int step = 128; step > 0; step >>= 1) {
+        for (int k = 7; k >= 0; --k) {
 #pragma unroll
-            for (int q = 0; q < kRowsPerThread; ++q) bin[q] += (uf[32 * (bin[q] + step - 1)] <= x[q]) ? step : 0;
+            for (int q = 0; q < kRowsPerThread; ++q) {
+                const uint32_t key_u =
+                    *reinterpret_cast<const uint32_t *>(uf + (b[q] << (k + 8)) + 128u * ((1u << k) - 1u));
+                b[q] = search_step(b[q], key_u, kx1[q]);
+            }
         }
 #pragma unroll
         for (int q = 0; q < kRowsPerThread; ++q) {
             if (r0 + q >= R) break;
-            uint32_t b = bin[q];
-            if (x[q] != x[q]) b = nan_bin;
-            if (f >= nf) b = 0;
-            Xb[(r0 + q) * stride + f] = (uint8_t)b;
+            uint32_t v = b[q];
+            if (x[q] != x[q]) v = nan_bin;
+            if (f >= nf) v = 0;
+            Xb[(r0 + q) * stride + f] = (uint8_t)v;
         }
     }
 }

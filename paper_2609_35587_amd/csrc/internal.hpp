@@ -89,6 +89,28 @@ hipError_t launch_topk(const float *scores, const int64_t *seg, int32_t P, int32
 hipError_t launch_regret(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx,
                          int32_t k, float *r1, float *rk, int32_t *best, hipStream_t s);
 
+// Order-preserving map of fp32 to uint32 (x < y <=> key(x) < key(y) for
+// non-NaN values; -0 must be normalised to +0 first).
+__device__ __forceinline__ uint32_t order_key(float v)
+{
+    const uint32_t u = __float_as_uint(v);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// One step of the bit-serial search: b <- 2 b + (key_u < kx1), i.e. + (u <= x)
+// with kx1 = key(x) + 1.  Subtract-with-borrow leaves the comparison in VCC,
+// add-with-carry shifts it in.
+__device__ __forceinline__ uint32_t search_step(uint32_t b, uint32_t key_u, uint32_t kx1)
+{
+    uint32_t out;
+    asm("v_sub_co_u32_e32 %0, vcc, %1, %2\n\t"
+        "v_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
+        : "=&v"(out)
+        : "v"(key_u), "v"(kx1), "v"(b)
+        : "vcc");
+    return out;
+}
+
 // Last segment p with seg[p] <= r (segments are [seg[p], seg[p+1])); the
 // result is always in [0, P-1], whatever the offsets hold.
 __device__ inline int32_t segment_of_row(const int64_t *__restrict__ seg, int32_t P, int64_t r)
