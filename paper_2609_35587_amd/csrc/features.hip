@@ -312,9 +312,8 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
                                                                  int nf, uint32_t nan_bin, uint8_t *__restrict__ Xb,
                                                                  int stride)
 {
-    __shared__ uint32_t u[128 * kFbStride];   // thresholds as order-preserving keys
-    for (int e = threadIdx.x; e < nf * kFbSlots; e += kFbThreads)
-        u[(e >> 8) * kFbStride + (e & 255)] = order_key(U[e]);
+    __shared__ float u[128 * kFbStride];
+    for (int e = threadIdx.x; e < nf * kFbSlots; e += kFbThreads) u[(e >> 8) * kFbStride + (e & 255)] = U[e];
     __syncthreads();
     constexpr int kPass = F % 64 == 0 ? 64 : 32;      // columns per evaluation of the map
     for (int64_t r = (int64_t)blockIdx.x * kFbThreads + threadIdx.x; r < R; r += (int64_t)gridDim.x * kFbThreads) {
@@ -337,27 +336,16 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
 #pragma unroll
             for (int f0 = p0; f0 < p0 + kPass; f0 += kFbChains) {
                 if (f0 < nf) {
-                    // b = #{u <= x} built from the top bit (the forest's own
-                    // binning search): at step k the probe is threshold
-                    // (b << (k + 1)) + 2^k - 1 of feature f0 + q
-                    uint32_t b[kFbChains], kx1[kFbChains];
+                    uint32_t b[kFbChains];
+#pragma unroll
+                    for (int q = 0; q < kFbChains; ++q) b[q] = (uint32_t)(f0 + q) * kFbStride;
+#pragma unroll
+                    for (int step = 128; step > 0; step >>= 1)
+#pragma unroll
+                        for (int q = 0; q < kFbChains; ++q) b[q] += (u[b[q] + step - 1] <= x[f0 + q]) ? step : 0;
 #pragma unroll
                     for (int q = 0; q < kFbChains; ++q) {
-                        b[q] = 0;
-                        kx1[q] = order_key(x[f0 + q] == 0.0f ? 0.0f : x[f0 + q]) + 1u;
-                    }
-                    const uint8_t *ub = reinterpret_cast<const uint8_t *>(u);
-#pragma unroll
-                    for (int k = 7; k >= 0; --k)
-#pragma unroll
-                        for (int q = 0; q < kFbChains; ++q) {
-                            const uint32_t off = (uint32_t)(f0 + q) * kFbStride * 4u + 4u * ((1u << k) - 1u);
-                            b[q] = search_step(b[q], *reinterpret_cast<const uint32_t *>(ub + (b[q] << (k + 3)) + off),
-                                               kx1[q]);
-                        }
-#pragma unroll
-                    for (int q = 0; q < kFbChains; ++q) {
-                        uint32_t v = b[q];
+                        uint32_t v = b[q] - (uint32_t)(f0 + q) * kFbStride;
                         if (x[f0 + q] != x[f0 + q]) v = nan_bin;
                         if (f0 + q >= nf) v = 0;
                         word[(f0 + q) / 4] |= v << (8 * ((f0 + q) % 4));
