@@ -229,6 +229,16 @@ __device__ __forceinline__ void fragments_landed()
     asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
 }
 
+// Between a block's last products and the first vector instruction reading
+// their results: a scheduling barrier and 32 wait states, so that no read of
+// an accumulator can be placed before the matrix core has written it.
+__device__ __forceinline__ void products_done()
+{
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // A ring slot may be refilled once this wave's reads of it have completed.
 __device__ __forceinline__ void reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
 
@@ -299,6 +309,7 @@ __device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const u
 #pragma unroll 1
         for (int ks = 4; ks < KS; ks += 4) trip(ks);
     }
+    products_done();
 }
 
 // acc[mt][nt] = init[mt] + products of the wave's two consecutive M-tiles
@@ -356,6 +367,7 @@ __device__ __forceinline__ void mma_block_mt2(const bf16x8 *__restrict__ W0, con
         step(2, ks + 1, false);
         refill(2, ks + 3);
     }
+    products_done();
 }
 
 // Bias of one 32-unit M-tile starting at unit u0, in accumulator layout.
