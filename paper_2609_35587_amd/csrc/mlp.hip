@@ -13,10 +13,11 @@
 //     per row goes out.
 //   * Each layer is computed transposed, H_l^T = W_l * H_{l-1}^T: the A
 //     operand is weights, pre-arranged into MFMA fragment order so every
-//     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all), sent
-//     by DMA loads straight into a 4-slot LDS ring per wave; the B operand is
-//     16 bytes of one activation row from LDS; the accumulator tile gives each
-//     lane 4 runs of 4 consecutive units of one row.
+//     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all),
+//     loaded into registers 8 k-steps ahead in the 512-unit layers and sent
+//     by DMA loads into a 4-slot LDS ring per wave in the last layer; the B
+//     operand is 16 bytes of one activation row from LDS; the accumulator
+//     tile gives each lane 4 runs of 4 consecutive units of one row.
 //   * Waves split the output units of a layer, so every weight is read once
 //     per tile; in a 512-unit layer a wave's two M-tiles share every
 //     activation fragment read.  A layer's results wait in registers until
@@ -315,21 +316,24 @@ __device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const u
 // acc[mt][nt] = init[mt] + products of the wave's two consecutive M-tiles
 // (fragments at W0 and W0 + KS fragments) with 4 N-tiles: every activation
 // fragment read serves two products and every weight fragment four.  The
-// ring holds both M-tiles' fragments of two k-steps; each k-step's pair is
-// refilled with the k-step two ahead once its reads have returned.
-template <int K_IN>
-__device__ __forceinline__ void mma_block_mt2(const bf16x8 *__restrict__ W0, const uint8_t *act, int row_bytes,
-                                              int lane, uint32_t ring, const uint8_t *ring_ptr,
-                                              const f32x16 &init0, const f32x16 &init1, f32x16 (&acc)[2][4])
+// weight fragments are loaded straight into registers PF k-steps ahead.
+template <int K_IN, int PF>
+__device__ __forceinline__ void mma_block_mt2_direct(const bf16x8 *__restrict__ W0, const uint8_t *act, int row_bytes,
+                                                     int lane, const f32x16 &init0, const f32x16 &init1,
+                                                     f32x16 (&acc)[2][4])
 {
     constexpr int KS = K_IN / 16;
-    static_assert(KS % 2 == 0, "k loop");
+    static_assert(KS % PF == 0, "k loop");
     const uint8_t *brow = act + (lane & 31) * row_bytes;
     const int sw = lane & 15, half = lane >> 5;
     const bf16x8 *w0 = W0 + lane, *w1 = W0 + KS * 64 + lane;
-    auto step = [&](int slot, int ks, bool first) {
-        const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
-        const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(ring_ptr + (slot + 1) * 1024 + lane * 16);
+    bf16x8 a0[PF], a1[PF];
+#pragma unroll
+    for (int j = 0; j < PF; ++j) {
+        a0[j] = w0[j * 64];
+        a1[j] = w1[j * 64];
+    }
+    auto step = [&](int j, int ks, bool first) {
         const int chunk = (((2 * ks + half) ^ sw) & 15) | ((2 * ks + half) & ~15);
         bf16x8 b[4];
 #pragma unroll
@@ -337,35 +341,20 @@ __device__ __forceinline__ void mma_block_mt2(const bf16x8 *__restrict__ W0, con
             b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
-            acc[0][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b[nt], first ? init0 : acc[0][nt], 0, 0, 0);
-            acc[1][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b[nt], first ? init1 : acc[1][nt], 0, 0, 0);
+            acc[0][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[j], b[nt], first ? init0 : acc[0][nt], 0, 0, 0);
+            acc[1][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[j], b[nt], first ? init1 : acc[1][nt], 0, 0, 0);
+        }
+        if (ks + PF < KS) {
+            a0[j] = w0[(ks + PF) * 64];
+            a1[j] = w1[(ks + PF) * 64];
         }
     };
-    auto refill = [&](int slot, int ks_next) {
-        if (ks_next < KS) {
-            reads_done();
-            dma_fragment(w0 + ks_next * 64, ring + slot * 1024);
-            dma_fragment(w1 + ks_next * 64, ring + (slot + 1) * 1024);
-            fragments_landed<2>();
-        } else {
-            fragments_landed<0>();
-        }
-    };
-    dma_fragment(w0, ring);
-    dma_fragment(w1, ring + 1024);
-    dma_fragment(w0 + 64, ring + 2048);
-    dma_fragment(w1 + 64, ring + 3072);
-    fragments_landed<2>();
-    step(0, 0, true);
-    refill(0, 2);
-    step(2, 1, false);
-    refill(2, 3);
+#pragma unroll
+    for (int j = 0; j < PF; ++j) step(j, j, j == 0);
 #pragma unroll 1
-    for (int ks = 2; ks < KS; ks += 2) {
-        step(0, ks, false);
-        refill(0, ks + 2);
-        step(2, ks + 1, false);
-        refill(2, ks + 3);
+    for (int ks = PF; ks < KS; ks += PF) {
+#pragma unroll
+        for (int j = 0; j < PF; ++j) step(j, ks + j, false);
     }
     products_done();
 }
@@ -407,8 +396,8 @@ __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const f
     uint2 staged[2][4][4];
     {
         f32x16 acc[2][4];
-        mma_block_mt2<K_IN>(Wf + (int64_t)(2 * wave) * KS * 64, act, in_row_bytes, lane, ring, ring_ptr,
-                            bias_tile(bias, 64 * wave, lane), bias_tile(bias, 64 * wave + 32, lane), acc);
+        mma_block_mt2_direct<K_IN, 8>(Wf + (int64_t)(2 * wave) * KS * 64, act, in_row_bytes, lane,
+                                      bias_tile(bias, 64 * wave, lane), bias_tile(bias, 64 * wave + 32, lane), acc);
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
