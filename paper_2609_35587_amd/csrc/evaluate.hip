@@ -83,6 +83,7 @@ __global__ __launch_bounds__(kEvalThreads) void k_eval_groups(const float *__res
 {
     __shared__ double red[kEvalThreads];
     const int32_t p = blockIdx.x;
+    if (p >= P) return;                                   // one workgroup per problem
     const int64_t base = seg[p], n = seg[p + 1] - seg[p];
     if (n <= 0) {
         if (threadIdx.x == 0) {

@@ -389,8 +389,7 @@ __device__ __forceinline__ uint2 gelu_group(const f32x16 &acc, int g)
 // layer input, then overwrite it in place.
 template <int K_IN>
 __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const float *__restrict__ bias,
-                                          uint8_t *act, int in_row_bytes, int wave, int lane, uint32_t ring,
-                                          const uint8_t *ring_ptr)
+                                          uint8_t *act, int in_row_bytes, int wave, int lane)
 {
     constexpr int KS = K_IN / 16;
     uint2 staged[2][4][4];
@@ -456,8 +455,8 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
     const bf16x8 *W1f = packed;
     const bf16x8 *W2f = W1f + kFrag1 * 64;
     const bf16x8 *W3f = W2f + kFrag2 * 64;
-    hidden512<128>(W1f, m.b1, act, 256, wave, lane, ring, ring_ptr);     // layer 1: 128 -> 512
-    hidden512<512>(W2f, m.b2, act, 1024, wave, lane, ring, ring_ptr);    // layer 2: 512 -> 512
+    hidden512<128>(W1f, m.b1, act, 256, wave, lane);     // layer 1: 128 -> 512
+    hidden512<512>(W2f, m.b2, act, 1024, wave, lane);    // layer 2: 512 -> 512
 
     // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two N-tiles),
     // GELU, bf16, then the 256 -> 1 dot product
