@@ -325,7 +325,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
     __shared__ __attribute__((aligned(16))) uint8_t lds[CHUNK_B + kTileRows * kStride];
     const float *leaves = reinterpret_cast<const float *>(lds + NODE_B);
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int t = lane % TC, s = lane / TC;
     // The children pair of node n is the word at n * ROW_B + col.
     constexpr uint32_t ROW_B = pair_row_bytes(TC);
@@ -360,15 +360,30 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
         const uint32_t p2 = D >= 3 ? *reinterpret_cast<const uint32_t *>(lds + 2 * ROW_B + col) : 0u;
         const uint32_t p3 = D >= 3 ? *reinterpret_cast<const uint32_t *>(lds + 3 * ROW_B + col) : 0u;
         uint4 pre[kVec];
+        const bool full_rows = stride == 128;              // wave-uniform
+        // A lane's byte offsets within its wave's slice are the same for every
+        // tile; only whole slices inside the row range skip the row guards.
         auto fetch = [&](int64_t t0) {
             const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
-            const int64_t n = r_end - w0;                  // rows of this wave left (may be <= 0)
+            const uint8_t *slice = Xb + w0 * stride;       // wave-uniform
+            if (full_rows && w0 + ROWS_PER_WAVE <= r_end) {
+                // 128-byte rows, all in range: chunk e % 8 of row e / 8
 #pragma unroll
-            for (int q = 0; q < kVec; ++q) {
-                const int e = lane + 64 * q;
-                const int rr = e / vpr, w = e - rr * vpr;
-                pre[q] = (rr < ROWS_PER_WAVE && rr < n) ? reinterpret_cast<const uint4 *>(Xb + (w0 + rr) * stride)[w]
-                                                        : make_uint4(0, 0, 0, 0);
+                for (int q = 0; q < kVec; ++q) {
+                    const int e = lane + 64 * q;
+                    if ((ROWS_PER_WAVE * 8) % 64 == 0 || e < ROWS_PER_WAVE * 8)
+                        pre[q] = *reinterpret_cast<const uint4 *>(slice + (e >> 3) * 128 + 16 * (e & 7));
+                }
+            } else {
+                const int n = (int)(r_end - w0 > 0 ? r_end - w0 : 0);   // rows of this slice left
+#pragma unroll
+                for (int q = 0; q < kVec; ++q) {
+                    const int e = lane + 64 * q;
+                    const int rr = e / vpr, w = e - rr * vpr;
+                    pre[q] = (rr < ROWS_PER_WAVE && rr < n)
+                                 ? *reinterpret_cast<const uint4 *>(slice + rr * stride + 16 * w)
+                                 : make_uint4(0, 0, 0, 0);
+                }
             }
         };
         fetch(r_begin);
@@ -376,17 +391,26 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
             const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
             // The previous rows' reads have all returned (their results were
             // used), so the region can be overwritten.
+            auto put = [&](int q, int rr, int w) {
+                if constexpr (kStride % 16 == 0) {
+                    *reinterpret_cast<uint4 *>(region + rr * kStride + 16 * w) = pre[q];
+                } else {
+                    uint32_t *d = reinterpret_cast<uint32_t *>(region + rr * kStride + 16 * w);
+                    d[0] = pre[q].x; d[1] = pre[q].y; d[2] = pre[q].z; d[3] = pre[q].w;
+                }
+            };
+            if (full_rows) {
 #pragma unroll
-            for (int q = 0; q < kVec; ++q) {
-                const int e = lane + 64 * q;
-                const int rr = e / vpr, w = e - rr * vpr;
-                if (rr < ROWS_PER_WAVE) {
-                    if constexpr (kStride % 16 == 0) {
-                        *reinterpret_cast<uint4 *>(region + rr * kStride + 16 * w) = pre[q];
-                    } else {
-                        uint32_t *d = reinterpret_cast<uint32_t *>(region + rr * kStride + 16 * w);
-                        d[0] = pre[q].x; d[1] = pre[q].y; d[2] = pre[q].z; d[3] = pre[q].w;
-                    }
+                for (int q = 0; q < kVec; ++q) {
+                    const int e = lane + 64 * q;
+                    if ((ROWS_PER_WAVE * 8) % 64 == 0 || e < ROWS_PER_WAVE * 8) put(q, e >> 3, e & 7);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < kVec; ++q) {
+                    const int e = lane + 64 * q;
+                    const int rr = e / vpr, w = e - rr * vpr;
+                    if (rr < ROWS_PER_WAVE) put(q, rr, w);
                 }
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the region is written before any lane reads it
