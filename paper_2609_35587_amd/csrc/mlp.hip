@@ -432,18 +432,34 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
     const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_address(ring_ptr));
     const int64_t row0 = (int64_t)blockIdx.x * kTile;
 
-    // input: standardise (fp32, two operations), NaN/inf read as 0, bf16
-    for (int e = threadIdx.x; e < kTile * 32; e += 64 * kMWaves) {
-        const int r = e >> 5, c4 = (e & 31) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row0 + r < R) v = *reinterpret_cast<const float4 *>(X + (row0 + r) * ld + c4);
+    // input: standardise (fp32, two operations), NaN/inf read as 0, bf16.
+    // A thread takes the same four columns of 8 rows 16 apart; all 8 loads
+    // are issued before the first is used, so the tile costs one trip to HBM.
+    {
+        constexpr int kXLoads = kTile * 32 / (64 * kMWaves);
+        static_assert(kXLoads * 64 * kMWaves == kTile * 32, "X staging covers the tile");
+        const int r_first = threadIdx.x >> 5, c4 = (threadIdx.x & 31) * 4;
+        constexpr int kRowStep = 64 * kMWaves / 32;
         const float4 mu = *reinterpret_cast<const float4 *>(m.mean + c4);
         const float4 is = *reinterpret_cast<const float4 *>(m.inv_std + c4);
-        const float z0 = ((__builtin_isfinite(v.x) ? v.x : 0.0f) - mu.x) * is.x;
-        const float z1 = ((__builtin_isfinite(v.y) ? v.y : 0.0f) - mu.y) * is.y;
-        const float z2 = ((__builtin_isfinite(v.z) ? v.z : 0.0f) - mu.z) * is.z;
-        const float z3 = ((__builtin_isfinite(v.w) ? v.w : 0.0f) - mu.w) * is.w;
-        *reinterpret_cast<uint2 *>(act + act_offset(r, 256, c4)) = make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
+        float4 v[kXLoads];
+#pragma unroll
+        for (int i = 0; i < kXLoads; ++i) {
+            // rows past R (R >= 1) read row R - 1 and are zeroed below: no
+            // branch splits the batch of loads
+            const int64_t r = row0 + r_first + kRowStep * i;
+            v[i] = *reinterpret_cast<const float4 *>(X + (r < R ? r : R - 1) * ld + c4);
+        }
+#pragma unroll
+        for (int i = 0; i < kXLoads; ++i) {
+            const bool in = row0 + r_first + kRowStep * i < R;
+            const float z0 = ((in && __builtin_isfinite(v[i].x) ? v[i].x : 0.0f) - mu.x) * is.x;
+            const float z1 = ((in && __builtin_isfinite(v[i].y) ? v[i].y : 0.0f) - mu.y) * is.y;
+            const float z2 = ((in && __builtin_isfinite(v[i].z) ? v[i].z : 0.0f) - mu.z) * is.z;
+            const float z3 = ((in && __builtin_isfinite(v[i].w) ? v[i].w : 0.0f) - mu.w) * is.w;
+            *reinterpret_cast<uint2 *>(act + act_offset(r_first + kRowStep * i, 256, c4)) =
+                make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
+        }
     }
     __syncthreads();
 
