@@ -328,6 +328,10 @@ __device__ __forceinline__ void mma_block_mt2_direct(const bf16x8 *__restrict__ 
         a0[j] = w0[j * 64];
         a1[j] = w1[j * 64];
     }
+    // keep the first PF k-steps' loads here: in a fully unrolled layer the
+    // scheduler would otherwise sink each next to its first use and wait on
+    // every one
+    __builtin_amdgcn_sched_barrier(0);
     auto step = [&](int j, int ks, bool first) {
         const int chunk = (((2 * ks + half) ^ sw) & 15) | ((2 * ks + half) & ~15);
         bf16x8 b[4];
@@ -421,95 +425,146 @@ __device__ __forceinline__ void hidden512(const bf16x8 *__restrict__ Wf, const f
     __syncthreads();
 }
 
+// X of one 128-row tile as a thread stages it: the same four columns of 8
+// rows 16 apart, plus the standardisation of those columns.  All loads are
+// issued together; X is read once, so its loads bypass the caches' retention
+// (non-temporal) and leave L2 to the weight fragments.
+constexpr int kXLoads = kTile * 32 / (64 * kMWaves);
+constexpr int kXRowStep = 64 * kMWaves / 32;
+static_assert(kXLoads * 64 * kMWaves == kTile * 32, "X staging covers the tile");
+
+struct XTile {
+    float4 mu, is, v[kXLoads];
+};
+
+__device__ __forceinline__ void load_x(const hwsel_mlp_t &m, const float *__restrict__ X, int64_t R, int64_t ld,
+                                       int64_t row0, int tid, XTile &t)
+{
+    typedef float f32x4_v __attribute__((ext_vector_type(4)));
+    const int r_first = tid >> 5, c4 = (tid & 31) * 4;
+    t.mu = *reinterpret_cast<const float4 *>(m.mean + c4);
+    t.is = *reinterpret_cast<const float4 *>(m.inv_std + c4);
+#pragma unroll
+    for (int i = 0; i < kXLoads; ++i) {
+        // rows past R (R >= 1) read row R - 1 and are zeroed when staged: no
+        // branch splits the batch of loads
+        const int64_t r = row0 + r_first + kXRowStep * i;
+        const f32x4_v x = __builtin_nontemporal_load(reinterpret_cast<const f32x4_v *>(X + (r < R ? r : R - 1) * ld + c4));
+        t.v[i] = make_float4(x.x, x.y, x.z, x.w);
+    }
+}
+
+// Standardise (fp32, two operations; NaN/inf read as 0), round to bf16 and
+// write the tile's input activations.
+__device__ __forceinline__ void stage_x(const XTile &t, int64_t row0, int64_t R, int tid, uint8_t *act)
+{
+    const int r_first = tid >> 5, c4 = (tid & 31) * 4;
+#pragma unroll
+    for (int i = 0; i < kXLoads; ++i) {
+        const bool in = row0 + r_first + kXRowStep * i < R;
+        const float4 v = t.v[i];
+        const float z0 = ((in && __builtin_isfinite(v.x) ? v.x : 0.0f) - t.mu.x) * t.is.x;
+        const float z1 = ((in && __builtin_isfinite(v.y) ? v.y : 0.0f) - t.mu.y) * t.is.y;
+        const float z2 = ((in && __builtin_isfinite(v.z) ? v.z : 0.0f) - t.mu.z) * t.is.z;
+        const float z3 = ((in && __builtin_isfinite(v.w) ? v.w : 0.0f) - t.mu.w) * t.is.w;
+        *reinterpret_cast<uint2 *>(act + act_offset(r_first + kXRowStep * i, 256, c4)) =
+            make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
+    }
+}
+
+// Persistent: one workgroup per compute unit walks the tiles blockIdx.x,
+// blockIdx.x + gridDim.x, ...  The next tile's X is requested as soon as the
+// current tile's last weight fragment has landed, so that its trip to HBM
+// overlaps the last epilogue and the row sums instead of starting the tile.
 __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, const bf16x8 *__restrict__ packed,
                                                               const float *__restrict__ X, int64_t R, int64_t ld,
                                                               float *__restrict__ scores)
 {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
     uint8_t *act = lds;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint8_t *ring_ptr = lds + kActBytes + wave * kRingBytes;
     const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_address(ring_ptr));
-    const int64_t row0 = (int64_t)blockIdx.x * kTile;
-
-    // input: standardise (fp32, two operations), NaN/inf read as 0, bf16.
-    // A thread takes the same four columns of 8 rows 16 apart; all 8 loads
-    // are issued before the first is used, so the tile costs one trip to HBM.
-    {
-        constexpr int kXLoads = kTile * 32 / (64 * kMWaves);
-        static_assert(kXLoads * 64 * kMWaves == kTile * 32, "X staging covers the tile");
-        const int r_first = threadIdx.x >> 5, c4 = (threadIdx.x & 31) * 4;
-        constexpr int kRowStep = 64 * kMWaves / 32;
-        const float4 mu = *reinterpret_cast<const float4 *>(m.mean + c4);
-        const float4 is = *reinterpret_cast<const float4 *>(m.inv_std + c4);
-        float4 v[kXLoads];
-#pragma unroll
-        for (int i = 0; i < kXLoads; ++i) {
-            // rows past R (R >= 1) read row R - 1 and are zeroed below: no
-            // branch splits the batch of loads
-            const int64_t r = row0 + r_first + kRowStep * i;
-            v[i] = *reinterpret_cast<const float4 *>(X + (r < R ? r : R - 1) * ld + c4);
-        }
-#pragma unroll
-        for (int i = 0; i < kXLoads; ++i) {
-            const bool in = row0 + r_first + kRowStep * i < R;
-            const float z0 = ((in && __builtin_isfinite(v[i].x) ? v[i].x : 0.0f) - mu.x) * is.x;
-            const float z1 = ((in && __builtin_isfinite(v[i].y) ? v[i].y : 0.0f) - mu.y) * is.y;
-            const float z2 = ((in && __builtin_isfinite(v[i].z) ? v[i].z : 0.0f) - mu.z) * is.z;
-            const float z3 = ((in && __builtin_isfinite(v[i].w) ? v[i].w : 0.0f) - mu.w) * is.w;
-            *reinterpret_cast<uint2 *>(act + act_offset(r_first + kRowStep * i, 256, c4)) =
-                make_uint2(pack_bf16x2(z0, z1), pack_bf16x2(z2, z3));
-        }
-    }
-    __syncthreads();
-
+    const int64_t n_tiles = (R + kTile - 1) / kTile;
     const bf16x8 *W1f = packed;
     const bf16x8 *W2f = W1f + kFrag1 * 64;
     const bf16x8 *W3f = W2f + kFrag2 * 64;
-    hidden512<128>(W1f, m.b1, act, 256, wave, lane);     // layer 1: 128 -> 512
-    hidden512<512>(W2f, m.b2, act, 1024, wave, lane);    // layer 2: 512 -> 512
+    const float b4 = m.b4[0];
+    XTile xt;
+    load_x(m, X, R, ld, (int64_t)blockIdx.x * kTile, (int)threadIdx.x, xt);
+    // A tile's row scores are stored only after the next tile's X has
+    // landed: the X wait would otherwise also wait for the stores.
+    float pending = 0.0f;
+    int64_t pending_row = -1;
+    for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+        // lane-derived addresses are recomputed per tile rather than hoisted
+        // out of the loop and held through the hidden layers
+        int ln = lane, tid = threadIdx.x;
+        asm volatile("" : "+v"(ln), "+v"(tid));
+        const int64_t row0 = tile * kTile;
+        stage_x(xt, row0, R, tid, act);
+        if (pending_row >= 0) scores[pending_row] = pending;
+        __syncthreads();
+        hidden512<128>(W1f, m.b1, act, 256, wave, ln);     // layer 1: 128 -> 512
+        hidden512<512>(W2f, m.b2, act, 1024, wave, ln);    // layer 2: 512 -> 512
 
-    // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two N-tiles),
-    // GELU, bf16, then the 256 -> 1 dot product
-    float part[4] = {0.f, 0.f, 0.f, 0.f};
-    const f32x16 b3 = bias_tile(m.b3, 32 * wave, lane);
-    // epilogue group q of a block of two N-tiles: GELU, bf16, dot with W4
-    auto epilogue = [&](const f32x16 (&acc)[2], int blk, int q) {
-        const int nt = q & 1, g = q >> 1;
-        const uint2 w = *reinterpret_cast<const uint2 *>(m.W4 + 32 * wave + 8 * g + 4 * (lane >> 5));
-        const uint2 y = gelu_group(acc[nt], g);
-        float p = part[2 * blk + nt];
-        p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
-        p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
-        p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
-        p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
-        part[2 * blk + nt] = p;
-    };
-    {
-        f32x16 accA[2], accB[2];
-        mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 0, lane, ring, ring_ptr, b3, accA);
-        mma_block<512, 2, true>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2, lane, ring, ring_ptr, b3, accB,
-                                [&](int h) {
-                                    if (h % 2 == 0) epilogue(accA, 0, h / 2);
-                                });
+        // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two
+        // N-tiles), GELU, bf16, then the 256 -> 1 dot product
+        float part[4] = {0.f, 0.f, 0.f, 0.f};
+        const f32x16 b3 = bias_tile(m.b3, 32 * wave, ln);
+        // the wave's W4 values, read before the fragment ring starts: a load
+        // among the ring's would make the compiler wait on the ring's loads
+        uint2 w4[4];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) epilogue(accB, 1, q);
-    }
-    // per-row partial sums: lanes l and l + 32 hold the same row; the wave's
-    // slot of the (now idle) fragment ring collects them
-    float *red = reinterpret_cast<float *>(lds + kActBytes);      // [wave][128], inside each wave's own ring
+        for (int g = 0; g < 4; ++g) w4[g] = *reinterpret_cast<const uint2 *>(m.W4 + 32 * wave + 8 * g + 4 * (ln >> 5));
+        // epilogue group q of a block of two N-tiles: GELU, bf16, dot with W4
+        auto epilogue = [&](const f32x16 (&acc)[2], int blk, int q) {
+            const int nt = q & 1, g = q >> 1;
+            const uint2 w = w4[g];
+            const uint2 y = gelu_group(acc[nt], g);
+            float p = part[2 * blk + nt];
+            p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
+            p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
+            p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
+            p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
+            part[2 * blk + nt] = p;
+        };
+        {
+            f32x16 accA[2], accB[2];
+            mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 0, ln, ring, ring_ptr, b3, accA);
+            mma_block<512, 2, true>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2, ln, ring, ring_ptr, b3, accB,
+                                    [&](int h) {
+                                        if (h % 2 == 0) epilogue(accA, 0, h / 2);
+                                    });
+            // every fragment of this tile has landed: the next tile's X
+            // loads can no longer delay a fragment wait.  Unconditional, so
+            // that the old tile's X is dead through the hidden layers; past
+            // the last tile the rows clamp to R - 1 and the values go unused.
+            load_x(m, X, R, ld, (tile + gridDim.x) * kTile, tid, xt);
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-        const float other = __shfl_xor(part[nt], 32, 64);
-        if (lane < 32) red[wave * (kRingBytes / 4) + 32 * nt + lane] = part[nt] + other;
-    }
-    __syncthreads();
-    if (threadIdx.x < kTile && row0 + threadIdx.x < R) {
-        float s = 0.0f;
+            for (int q = 0; q < 8; ++q) epilogue(accB, 1, q);
+        }
+        // per-row partial sums: lanes l and l + 32 hold the same row; the
+        // wave's slot of the (now idle) fragment ring collects them
+        float *red = reinterpret_cast<float *>(lds + kActBytes);      // [wave][128], inside each wave's own ring
 #pragma unroll
-        for (int w = 0; w < kMWaves; ++w) s += red[w * (kRingBytes / 4) + threadIdx.x];
-        scores[row0 + threadIdx.x] = s + m.b4[0];
+        for (int nt = 0; nt < 4; ++nt) {
+            const float other = __shfl_xor(part[nt], 32, 64);
+            if (ln < 32) red[wave * (kRingBytes / 4) + 32 * nt + ln] = part[nt] + other;
+        }
+        __syncthreads();
+        pending_row = -1;
+        if (threadIdx.x < kTile && row0 + threadIdx.x < R) {
+            float s = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kMWaves; ++w) s += red[w * (kRingBytes / 4) + threadIdx.x];
+            pending = s + b4;
+            pending_row = row0 + threadIdx.x;
+        }
+        // the next tile writes its input over act only; red (in the rings)
+        // is not refilled before that tile's last layer, several barriers on
     }
+    if (pending_row >= 0) scores[pending_row] = pending;
 }
 
 }  // namespace
@@ -534,7 +589,13 @@ hipError_t launch_mlp_pack(const hwsel_mlp_t &m, void *packed, hipStream_t s)
 hipError_t launch_mlp_packed(const hwsel_mlp_t &m, const void *packed, const float *X, int64_t R, int64_t ld,
                              float *scores, hipStream_t s)
 {
-    const dim3 grid((unsigned)((R + kTile - 1) / kTile)), block(64 * kMWaves);
+    // one persistent workgroup per compute unit (160 KB of LDS each)
+    int dev = 0, n_cu = 256;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+        n_cu = 256;
+    const int64_t n_tiles = (R + kTile - 1) / kTile;
+    const dim3 grid((unsigned)(n_tiles < n_cu ? n_tiles : n_cu)), block(64 * kMWaves);
     hipLaunchKernelGGL(k_mlp_mfma, grid, block, 0, s, m, static_cast<const bf16x8 *>(packed), X, R, ld, scores);
     return hipGetLastError();
 }
