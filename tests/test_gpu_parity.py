@@ -259,6 +259,37 @@ def test_mlp_ragged_and_nonfinite(R):
     _assert_mlp(g2, o)
 
 
+def test_mlp_persistent_tile_walk():
+    """513 tiles of 128 rows on at most 256 persistent workgroups: workgroups
+    walk 2 or 3 tiles, the last one ragged (77 rows).  Every row against the
+    fp32 row-block path, a sample (all of the last two tiles included)
+    against the oracle."""
+    R = 512 * 128 + 77
+    say(f"mlp persistent walk R={R}")
+    rng = np.random.default_rng(2609)
+    m = synth.mlp(synth.CONFIGS["mlp"])
+    md = {k: hwsel.to_device(v) for k, v in m.items()}
+    sd = np.where(m["inv_std"] > 0, 1.0 / np.where(m["inv_std"] > 0, m["inv_std"], 1.0), 1.0)
+    X = (rng.standard_normal((R, 128)) * sd + m["mean"]).astype(np.float32)
+    Xd = torch.from_numpy(X).cuda()
+    packed = hwsel.hwsel_mlp_pack(md)
+    s = hwsel.hwsel_mlp_score(md, Xd, packed=packed)
+    s_ref = hwsel.hwsel_mlp_score(md, Xd).double()
+    rms = float(torch.sqrt(torch.mean(s_ref ** 2)))
+    ratio = torch.abs(s.double() - s_ref) / (2e-2 * torch.clamp(torch.abs(s_ref), min=rms))
+    say("  max |diff| / (2e-2 max(|ref|, rms)) %.3g" % float(ratio.max()))
+    assert float(ratio.max()) <= 1.0
+    rows = np.unique(np.concatenate([rng.choice(R, 2048, replace=False), np.arange(R - 205, R)]))
+    g = s.cpu().numpy()[rows]
+    o = oracle.mlp(m, X[rows])
+    say("  oracle sample: max err/bound %.3g  rms %.3g" % _assert_mlp(g, o))
+    # the output holds exactly R scores: a row past R is never written
+    out = torch.full((R + 64,), 12345.0, device="cuda")
+    hwsel.hwsel_mlp_score(md, Xd, scores=out[:R], packed=packed)
+    assert bool((out[R:] == 12345.0).all())
+    assert bool((out[:R] == s).all())
+
+
 # ----------------------------------------------------------------------------
 # every packed traversal shape (depth 1..10, chunk widths 64/32/16), padding
 # trees, ragged row counts, NaN features with both default directions
