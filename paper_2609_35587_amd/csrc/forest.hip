@@ -186,17 +186,35 @@ __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict_
         u[bin_table_index(e >> 8, e & 255)] = order_key(U[e]);
     __syncthreads();
     const int f = threadIdx.x & 127;
-    const int sub = threadIdx.x >> 7;                 // 8 row lanes per block
+    // 8 row lanes per block; a wave's 64 threads share one, so the row
+    // arithmetic below stays scalar
+    const int sub = __builtin_amdgcn_readfirstlane(threadIdx.x >> 7);
     if (f >= stride) return;
     const uint8_t *uf = reinterpret_cast<const uint8_t *>(u + bin_table_index(f, 0));
     constexpr int kRowsPerThread = 8;                 // independent searches in flight
     const int64_t step_rows = (int64_t)gridDim.x * 8 * kRowsPerThread;
+    // the next group's values are requested before this group's searches,
+    // so the trip to HBM overlaps them
+    // Branch-free: rows past R read row R - 1 and columns past nf read
+    // column nf - 1 (R, nf >= 1); neither result is stored as such.
+    const int fc = f < nf ? f : nf - 1;
+    auto fetch = [&](int64_t r0, float (&x)[kRowsPerThread]) {
+#pragma unroll
+        for (int q = 0; q < kRowsPerThread; ++q) {
+            const int64_t r = r0 + q;
+            x[q] = X[(r < R ? r : R - 1) * ld + fc];
+        }
+    };
+    float xn[kRowsPerThread];
+    fetch(((int64_t)blockIdx.x * 8 + sub) * kRowsPerThread, xn);
     for (int64_t r0 = ((int64_t)blockIdx.x * 8 + sub) * kRowsPerThread; r0 < R; r0 += step_rows) {
         float x[kRowsPerThread];
         uint32_t kx1[kRowsPerThread], b[kRowsPerThread];
 #pragma unroll
+        for (int q = 0; q < kRowsPerThread; ++q) x[q] = xn[q];
+        fetch(r0 + step_rows, xn);
+#pragma unroll
         for (int q = 0; q < kRowsPerThread; ++q) {
-            x[q] = (f < nf && r0 + q < R) ? X[(r0 + q) * ld + f] : 0.0f;
             kx1[q] = order_key(x[q] == 0.0f ? 0.0f : x[q]) + 1u;
             b[q] = 0;
         }
