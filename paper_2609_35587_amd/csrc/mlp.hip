@@ -6,11 +6,12 @@
 //
 // Packed path (weights arranged once by hwsel_mlp_pack): the hidden layers
 // run on the bf16 matrix cores, v_mfma_f32_32x32x16_bf16.
-//   * A workgroup (8 waves) owns a tile of 128 rows.  The tile's activations
-//     stay in LDS as bf16 for the whole network ([row][unit], 16-byte chunks
-//     XOR-swizzled by row so that 16 consecutive rows at one logical chunk
-//     fall on 16 distinct 16-byte bank groups); only X comes in and one score
-//     per row goes out.
+//   * One persistent workgroup (8 waves) per compute unit walks tiles of
+//     128 rows.  A tile's activations stay in LDS as bf16 for the whole
+//     network ([row][unit], 16-byte chunks XOR-swizzled by row so that 16
+//     consecutive rows at one logical chunk fall on 16 distinct 16-byte bank
+//     groups); only X comes in, fetched while the previous tile's last layer
+//     finishes, and one score per row goes out.
 //   * Each layer is computed transposed, H_l^T = W_l * H_{l-1}^T: the A
 //     operand is weights, pre-arranged into MFMA fragment order so every
 //     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all),
