@@ -187,6 +187,9 @@ int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int6
  *                                            NaN and +-inf to 0)
  *   h_l = bf16(GELU(W_l h_{l-1} + b_l)), l = 1..3, fp32 accumulation
  *   score = W4 h3 + b4 in fp32.
+ * GELU(a) = a Phi(a) (the erf form).  The row-block kernel evaluates it with
+ * erff; the matrix-core kernel with a fitted approximation whose absolute
+ * error is below 1e-6 for every finite a (exactly max(a, 0) for |a| >= 20).
  * Device arrays: mean, inv_std fp32 [128]; W1 [512][128], W2 [512][512],
  * W3 [256][512], W4 [1][256] as bf16 bit patterns (uint16), row-major
  * [out][in]; b1..b4 fp32.  The struct itself is read on the host.
