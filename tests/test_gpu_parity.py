@@ -61,6 +61,26 @@ def test_forest_tiny_all_rows(tiny):
     assert np.array_equal(sp.view(np.uint32), sp2.view(np.uint32))      # run-to-run identical
 
 
+def test_features_and_forest_in_a_wider_matrix(tiny):
+    """X as the first 64 columns of a 76-column matrix: features land in those
+    columns only, bit-identical to a contiguous X, and both forest paths
+    score the strided X exactly as the contiguous one."""
+    w, d = tiny
+    say("features + forest, ld 76")
+    R = w.cands["tile_m"].shape[0]
+    wide = torch.full((R, 76), -7.0, dtype=torch.float32, device="cuda")
+    Xs = hwsel.hwsel_features(w.hw, d.problems, d.seg, d.cands, 64, X=wide[:, :64])
+    Xc = d.features(64)
+    assert Xs.stride(0) == 76
+    assert bool((Xs.view(torch.int32) == Xc.view(torch.int32)).all())
+    assert bool((wide[:, 64:] == -7.0).all())
+    packed = hwsel.hwsel_forest_pack(d.forest)
+    for pk in (None, packed):
+        a = hwsel.hwsel_forest_score(d.forest, Xs, packed=pk)
+        b = hwsel.hwsel_forest_score(d.forest, Xc, packed=pk)
+        assert bool((a.view(torch.int32) == b.view(torch.int32)).all())
+
+
 def _leaf_probe(forest: dict, t0: int) -> dict:
     """Same nodes, leaves zero except tree t0 whose leaf l holds the value l:
     the ensemble's score is exactly the leaf index reached in tree t0."""
@@ -288,6 +308,26 @@ def test_mlp_persistent_tile_walk():
     hwsel.hwsel_mlp_score(md, Xd, scores=out[:R], packed=packed)
     assert bool((out[R:] == 12345.0).all())
     assert bool((out[:R] == s).all())
+
+
+@pytest.mark.parametrize("ld", [136, 256])
+def test_mlp_strided_rows(ld):
+    """X with a row stride above 128 (a column slice of a wider matrix): both
+    kernels give exactly the scores of the contiguous copy."""
+    R = 3 * 128 + 5
+    say(f"mlp strided ld={ld}")
+    rng = np.random.default_rng(ld)
+    m = synth.mlp(synth.CONFIGS["mlp"])
+    md = {k: hwsel.to_device(v) for k, v in m.items()}
+    wide = torch.from_numpy(rng.standard_normal((R, ld)).astype(np.float32)).cuda()
+    Xs = wide[:, :128]
+    assert Xs.stride(0) == ld
+    Xc = Xs.contiguous()
+    packed = hwsel.hwsel_mlp_pack(md)
+    assert bool((hwsel.hwsel_mlp_score(md, Xs, packed=packed) == hwsel.hwsel_mlp_score(md, Xc, packed=packed)).all())
+    assert bool((hwsel.hwsel_mlp_score(md, Xs) == hwsel.hwsel_mlp_score(md, Xc)).all())
+    o = oracle.mlp(m, Xc.cpu().numpy())
+    _assert_mlp(hwsel.hwsel_mlp_score(md, Xs, packed=packed).cpu().numpy(), o)
 
 
 # ----------------------------------------------------------------------------
