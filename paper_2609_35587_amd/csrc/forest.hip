@@ -289,38 +289,7 @@ __device__ __forceinline__ void descend_root(int &node, uint32_t &code, uint32_t
     pair = p_out;
 }
 
-template <int CTRL, int ROW_MASK, bool ZERO_FILL>
-__device__ __forceinline__ float dpp_add(float v)
-{
-    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xf, ZERO_FILL));
-}
 
-// Sums over each aligned group of TC lanes (TC in {16, 32, 64}) of N
-// independent values with DPP: an inclusive scan inside 16-lane rows, then
-// row broadcasts.  The last lane of each group ends with the group's total,
-// always in the same order.  The values advance stage by stage so that the
-// dependent DPP steps of one are interleaved with the others'.
-template <int TC, int N>
-__device__ __forceinline__ void group_totals(float (&v)[N])
-{
-    static_assert(TC == 16 || TC == 32 || TC == 64, "group width");
-#pragma unroll
-    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x111, 0xf, true>(v[a]);
-#pragma unroll
-    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x112, 0xf, true>(v[a]);
-#pragma unroll
-    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x114, 0xf, true>(v[a]);
-#pragma unroll
-    for (int a = 0; a < N; ++a) v[a] = dpp_add<0x118, 0xf, true>(v[a]);
-    if constexpr (TC >= 32) {
-#pragma unroll
-        for (int a = 0; a < N; ++a) v[a] = dpp_add<0x142, 0xa, false>(v[a]);
-    }
-    if constexpr (TC >= 64) {
-#pragma unroll
-        for (int a = 0; a < N; ++a) v[a] = dpp_add<0x143, 0xc, false>(v[a]);
-    }
-}
 
 template <int TC, int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__restrict__ chunks, int n_chunks,
