@@ -15,16 +15,14 @@
 //   * Each layer is computed transposed, H_l^T = W_l * H_{l-1}^T: the A
 //     operand is weights, pre-arranged into MFMA fragment order so every
 //     fragment is one coalesced 1 KB load (L2-resident: 0.9 MB in all),
-//     loaded into registers 8 k-steps ahead in the 512-unit layers and sent
-//     by DMA loads into a 4-slot LDS ring per wave in the last layer; the B
-//     operand is 16 bytes of one activation row from LDS; the accumulator
-//     tile gives each lane 4 runs of 4 consecutive units of one row.
+//     loaded into registers ahead of use (8 k-steps in the 512-unit layers,
+//     4 in the last); the B operand is 16 bytes of one activation row from
+//     LDS; the accumulator tile gives each lane 4 runs of 4 consecutive
+//     units of one row.
 //   * Waves split the output units of a layer, so every weight is read once
 //     per tile; in a 512-unit layer a wave's two M-tiles share every
 //     activation fragment read.  A layer's results wait in registers until
 //     all waves have read the previous layer, then overwrite it in place.
-//     In the last layer the first block's epilogue runs on the vector units
-//     while the second block's products run on the matrix core.
 //   * GELU(a) = max(a, 0) - |a| Phi(-|a|) with Phi(-x) = 2^P(x), P a fitted
 //     degree-5 polynomial (|error| <= 6e-7, far below the bf16 rounding that
 //     follows).
@@ -145,8 +143,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kTile = 128;                    // rows per workgroup
 constexpr int kMWaves = 8;
 constexpr int kActBytes = kTile * 1024;       // 128 rows x 512 bf16 units
-constexpr int kRingBytes = 4 * 1024;          // per wave: four 1 KB weight fragments
-constexpr int kLdsBytes = kActBytes + kMWaves * kRingBytes;   // 160 KB
+constexpr int kRedFloats = kTile;             // per wave: one partial score per row
+constexpr int kLdsBytes = kActBytes + kMWaves * kRedFloats * 4;   // 132 KB
 // fragment counts (32 units x 16 inputs each) per layer
 constexpr int kFrag1 = (512 / 32) * (128 / 16);
 constexpr int kFrag2 = (512 / 32) * (512 / 16);
@@ -197,35 +195,6 @@ __device__ __forceinline__ int act_offset(int row, int row_bytes, int unit)
     return row * row_bytes + ((((unit >> 3) ^ row) & 15) | ((unit >> 3) & ~15)) * 16 + (unit & 7) * 2;
 }
 
-__device__ __forceinline__ uint32_t lds_address(const void *p)
-{
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
-}
-
-// Copy 16 bytes per lane from global memory straight into LDS at
-// lds_base + 16 * lane (one weight fragment per wave).  M0 carries the LDS
-// address and is restored afterwards.
-__device__ __forceinline__ void dma_fragment(const bf16x8 *g, uint32_t lds_base)
-{
-    uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\t"
-                 "s_mov_b32 m0, %1\n\t"
-                 "global_load_lds_dwordx4 %2, off\n\t"
-                 "s_mov_b32 m0, %0"
-                 : "=&s"(saved)
-                 : "s"(lds_base), "v"(g)
-                 : "memory");
-}
-
-// Loads complete in issue order; "at most N outstanding" means every load
-// older than the N most recent has landed (other loads in flight only make
-// this stricter).  The memory clobber keeps LDS reads after the wait.
-template <int N>
-__device__ __forceinline__ void fragments_landed()
-{
-    asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
-}
-
 // Between a block's last products and the first vector instruction reading
 // their results: a scheduling barrier and 32 wait states, so that no read of
 // an accumulator can be placed before the matrix core has written it.
@@ -234,79 +203,6 @@ __device__ __forceinline__ void products_done()
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
     __builtin_amdgcn_sched_barrier(0);
-}
-
-// A ring slot may be refilled once this wave's reads of it have completed.
-__device__ __forceinline__ void reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
-
-struct NoSide {
-    __device__ void operator()(int) const {}
-};
-
-// acc[nt] = init + sum over K_IN of W-fragments of one 32-unit M-tile x
-// activations of NB 32-row N-tiles starting at row 32*nt0.  `init` (the
-// bias in accumulator layout) enters as the first product's addend.  The
-// weight fragments stream through the wave's 4-slot LDS ring, two k-steps
-// ahead, four k-steps per trip.
-// `side(h)`, h = 0 .. K_IN/32 - 1, is independent vector work (the previous
-// block's epilogue) issued between the products of k-steps 2h and 2h+1 so
-// that it runs while the matrix core is busy; with side work the k loop is
-// unrolled, otherwise it is rolled after a peeled first trip.
-template <int K_IN, int NB, bool UNROLL = false, class Side = NoSide>
-__device__ __forceinline__ void mma_block(const bf16x8 *__restrict__ Wm, const uint8_t *act, int row_bytes,
-                                          int nt0, int lane, uint32_t ring, const uint8_t *ring_ptr,
-                                          const f32x16 &init, f32x16 (&acc)[NB], Side side = Side())
-{
-    constexpr int KS = K_IN / 16;
-    static_assert(KS % 4 == 0, "k loop");
-    const int r0 = (lane & 31) + 32 * nt0;
-    const uint8_t *brow = act + r0 * row_bytes;
-    const int sw = lane & 15, half = lane >> 5;
-    const bf16x8 *wp = Wm + lane;
-    auto step = [&](int slot, int ks, bool first) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ring_ptr + slot * 1024 + lane * 16);
-        const int chunk = (((2 * ks + half) ^ sw) & 15) | ((2 * ks + half) & ~15);
-        bf16x8 b[NB];
-#pragma unroll
-        for (int nt = 0; nt < NB; ++nt)
-            b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
-#pragma unroll
-        for (int nt = 0; nt < NB; ++nt)
-            acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[nt], first ? init : acc[nt], 0, 0, 0);
-    };
-    // refill slots first_slot, first_slot + 1 with k-steps ks_next, ks_next + 1
-    auto refill = [&](int first_slot, int ks_next) {
-        if (ks_next < KS) {
-            reads_done();
-            dma_fragment(wp + ks_next * 64, ring + first_slot * 1024);
-            dma_fragment(wp + (ks_next + 1) * 64, ring + (first_slot + 1) * 1024);
-            fragments_landed<2>();
-        } else if (first_slot == 0) {
-            fragments_landed<0>();
-        }
-    };
-    auto trip = [&](int ks) {
-        step(0, ks, ks == 0);
-        side(ks / 2);
-        step(1, ks + 1, false);
-        refill(0, ks + 4);
-        step(2, ks + 2, false);
-        side(ks / 2 + 1);
-        step(3, ks + 3, false);
-        refill(2, ks + 6);
-    };
-#pragma unroll
-    for (int q = 0; q < 4; ++q) dma_fragment(wp + q * 64, ring + q * 1024);
-    fragments_landed<2>();
-    if constexpr (UNROLL) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ks += 4) trip(ks);
-    } else {
-        trip(0);
-#pragma unroll 1
-        for (int ks = 4; ks < KS; ks += 4) trip(ks);
-    }
-    products_done();
 }
 
 // acc[mt][nt] = init[mt] + products of the wave's two consecutive M-tiles
@@ -348,6 +244,42 @@ __device__ __forceinline__ void mma_block_mt2_direct(const bf16x8 *__restrict__ 
             a0[j] = w0[(ks + PF) * 64];
             a1[j] = w1[(ks + PF) * 64];
         }
+    };
+#pragma unroll
+    for (int j = 0; j < PF; ++j) step(j, j, j == 0);
+#pragma unroll 1
+    for (int ks = PF; ks < KS; ks += PF) {
+#pragma unroll
+        for (int j = 0; j < PF; ++j) step(j, ks + j, false);
+    }
+    products_done();
+}
+
+// acc[nt] = init + products of one M-tile (fragments at W) with the 4
+// N-tiles; weight fragments loaded straight into registers PF k-steps ahead.
+template <int K_IN, int PF>
+__device__ __forceinline__ void mma_block_mt1_direct(const bf16x8 *__restrict__ W, const uint8_t *act, int row_bytes,
+                                                     int lane, const f32x16 &init, f32x16 (&acc)[4])
+{
+    constexpr int KS = K_IN / 16;
+    static_assert(KS % PF == 0, "k loop");
+    const uint8_t *brow = act + (lane & 31) * row_bytes;
+    const int sw = lane & 15, half = lane >> 5;
+    const bf16x8 *w = W + lane;
+    bf16x8 a[PF];
+#pragma unroll
+    for (int j = 0; j < PF; ++j) a[j] = w[j * 64];
+    __builtin_amdgcn_sched_barrier(0);
+    auto step = [&](int j, int ks, bool first) {
+        const int chunk = (((2 * ks + half) ^ sw) & 15) | ((2 * ks + half) & ~15);
+        bf16x8 b[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+            b[nt] = *reinterpret_cast<const bf16x8 *>(brow + nt * 32 * row_bytes + chunk * 16);
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+            acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j], b[nt], first ? init : acc[nt], 0, 0, 0);
+        if (ks + PF < KS) a[j] = w[(ks + PF) * 64];
     };
 #pragma unroll
     for (int j = 0; j < PF; ++j) step(j, j, j == 0);
@@ -484,8 +416,6 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
     uint8_t *act = lds;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint8_t *ring_ptr = lds + kActBytes + wave * kRingBytes;
-    const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_address(ring_ptr));
     const int64_t n_tiles = (R + kTile - 1) / kTile;
     const bf16x8 *W1f = packed;
     const bf16x8 *W2f = W1f + kFrag1 * 64;
@@ -509,61 +439,52 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
         hidden512<128>(W1f, m.b1, act, 256, wave, ln);     // layer 1: 128 -> 512
         hidden512<512>(W2f, m.b2, act, 1024, wave, ln);    // layer 2: 512 -> 512
 
-        // layer 3: 512 -> 256 (one M-tile per wave, two blocks of two
+        // layer 3: 512 -> 256 (one M-tile of 32 units per wave, all four
         // N-tiles), GELU, bf16, then the 256 -> 1 dot product
         float part[4] = {0.f, 0.f, 0.f, 0.f};
         const f32x16 b3 = bias_tile(m.b3, 32 * wave, ln);
-        // the wave's W4 values, read before the fragment ring starts: a load
-        // among the ring's would make the compiler wait on the ring's loads
+        // the W4 weights of the wave's 32 units
         uint2 w4[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) w4[g] = *reinterpret_cast<const uint2 *>(m.W4 + 32 * wave + 8 * g + 4 * (ln >> 5));
-        // epilogue group q of a block of two N-tiles: GELU, bf16, dot with W4
-        auto epilogue = [&](const f32x16 (&acc)[2], int blk, int q) {
-            const int nt = q & 1, g = q >> 1;
-            const uint2 w = w4[g];
-            const uint2 y = gelu_group(acc[nt], g);
-            float p = part[2 * blk + nt];
-            p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
-            p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
-            p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
-            p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
-            part[2 * blk + nt] = p;
-        };
         {
-            f32x16 accA[2], accB[2];
-            mma_block<512, 2>(W3f + (int64_t)wave * 32 * 64, act, 1024, 0, ln, ring, ring_ptr, b3, accA);
-            mma_block<512, 2, true>(W3f + (int64_t)wave * 32 * 64, act, 1024, 2, ln, ring, ring_ptr, b3, accB,
-                                    [&](int h) {
-                                        if (h % 2 == 0) epilogue(accA, 0, h / 2);
-                                    });
-            // every fragment of this tile has landed: the next tile's X
-            // loads can no longer delay a fragment wait.  Unconditional, so
-            // that the old tile's X is dead through the hidden layers; past
-            // the last tile the rows clamp to R - 1 and the values go unused.
-            load_x(m, X, R, ld, (tile + gridDim.x) * kTile, tid, xt);
+            f32x16 acc[4];
+            mma_block_mt1_direct<512, 4>(W3f + (int64_t)wave * 32 * 64, act, 1024, ln, b3, acc);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) epilogue(accB, 1, q);
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    // halfway through the epilogue (half the accumulators
+                    // free), request the next tile's X
+                    if (nt == 2 && g == 0) load_x(m, X, R, ld, (tile + gridDim.x) * kTile, tid, xt);
+                    const uint2 w = w4[g];
+                    const uint2 y = gelu_group(acc[nt], g);
+                    float p = part[nt];
+                    p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
+                    p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
+                    p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
+                    p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
+                    part[nt] = p;
+                }
         }
-        // per-row partial sums: lanes l and l + 32 hold the same row; the
-        // wave's slot of the (now idle) fragment ring collects them
-        float *red = reinterpret_cast<float *>(lds + kActBytes);      // [wave][128], inside each wave's own ring
+        // per-row partial sums: lanes l and l + 32 hold the same row
+        float *red = reinterpret_cast<float *>(lds + kActBytes);      // [wave][128]
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
             const float other = __shfl_xor(part[nt], 32, 64);
-            if (ln < 32) red[wave * (kRingBytes / 4) + 32 * nt + ln] = part[nt] + other;
+            if (ln < 32) red[wave * kRedFloats + 32 * nt + ln] = part[nt] + other;
         }
         __syncthreads();
         pending_row = -1;
         if (threadIdx.x < kTile && row0 + threadIdx.x < R) {
             float s = 0.0f;
 #pragma unroll
-            for (int w = 0; w < kMWaves; ++w) s += red[w * (kRingBytes / 4) + threadIdx.x];
+            for (int w = 0; w < kMWaves; ++w) s += red[w * kRedFloats + threadIdx.x];
             pending = s + b4;
             pending_row = row0 + threadIdx.x;
         }
-        // the next tile writes its input over act only; red (in the rings)
-        // is not refilled before that tile's last layer, several barriers on
+        // the next tile writes its input over act only; red is not written
+        // again before that tile's last layer, several barriers on
     }
     if (pending_row >= 0) scores[pending_row] = pending;
 }
