@@ -117,36 +117,67 @@ __global__ void k_catalogue_offsets(const int64_t *__restrict__ n_valid, int32_t
 
 constexpr int kCompactThreads = 1024;
 
+// Ordered compaction of one problem's mask (one workgroup per problem).  A
+// step covers kBlocks consecutive blocks of 1,024 four-byte words (4 points
+// each); thread i takes word i of every block, all loads issued together.
+// Within a wave, the valid points of lower lanes are counted from one ballot
+// per byte position (mbcnt); across the 16 waves and the blocks, the wave
+// totals meet in LDS.  Two barriers per step of 16,384 points.
+constexpr int kBlocks = 4;
+
 __global__ __launch_bounds__(kCompactThreads) void k_catalogue_compact(const uint8_t *__restrict__ mask,
                                                                        const int64_t *__restrict__ seg,
                                                                        int32_t *__restrict__ point, int64_t cap)
 {
-    __shared__ int32_t scan[kCompactThreads];
+    constexpr int kWavesC = kCompactThreads / 64;
+    __shared__ int32_t wave_total[kBlocks][kWavesC];
     const int32_t p = blockIdx.x;
+    const int wave = threadIdx.x >> 6;
     const uint32_t *row = reinterpret_cast<const uint32_t *>(mask + (int64_t)p * kCat);
     int64_t out = seg[p];
-    for (int64_t w0 = 0; w0 < kWords; w0 += kCompactThreads) {
-        const int64_t w = w0 + threadIdx.x;
-        const uint32_t word = w < kWords ? row[w] : 0u;
-        const int32_t c = (int32_t)((word & 1u) + ((word >> 8) & 1u) + ((word >> 16) & 1u) + ((word >> 24) & 1u));
-        scan[threadIdx.x] = c;
-        __syncthreads();
-        // inclusive Hillis-Steele scan
-        for (int s = 1; s < kCompactThreads; s <<= 1) {
-            const int32_t v = threadIdx.x >= s ? scan[threadIdx.x - s] : 0;
-            __syncthreads();
-            scan[threadIdx.x] += v;
-            __syncthreads();
-        }
-        int64_t pos = out + scan[threadIdx.x] - c;
+    for (int64_t w0 = 0; w0 < kWords; w0 += kBlocks * kCompactThreads) {
+        uint32_t word[kBlocks];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if ((word >> (8 * q)) & 1u) {
-                if (pos < cap) point[pos] = (int32_t)(4 * w + q);
-                ++pos;
+        for (int k = 0; k < kBlocks; ++k) {
+            const int64_t w = w0 + k * kCompactThreads + threadIdx.x;
+            word[k] = w < kWords ? row[w] : 0u;
+        }
+        int32_t below[kBlocks];              // valid points of block k in lower lanes of this wave
+#pragma unroll
+        for (int k = 0; k < kBlocks; ++k) {
+            int32_t bl = 0, total = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint64_t b = __ballot((word[k] >> (8 * q)) & 1u);
+                bl += (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+                total += __popcll(b);
             }
-        out += scan[kCompactThreads - 1];
-        __syncthreads();
+            below[k] = bl;
+            if ((threadIdx.x & 63) == 0) wave_total[k][wave] = total;
+        }
+        lds_barrier();
+        int64_t base = out;                  // points of the earlier blocks of this step
+#pragma unroll
+        for (int k = 0; k < kBlocks; ++k) {
+            int32_t before = 0, all = 0;
+#pragma unroll
+            for (int i = 0; i < kWavesC; ++i) {
+                const int32_t t = wave_total[k][i];
+                before += i < wave ? t : 0;
+                all += t;
+            }
+            int64_t pos = base + before + below[k];
+            const int64_t w = w0 + k * kCompactThreads + threadIdx.x;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if ((word[k] >> (8 * q)) & 1u) {
+                    if (pos < cap) point[pos] = (int32_t)(4 * w + q);
+                    ++pos;
+                }
+            base += all;
+        }
+        out = base;
+        lds_barrier();                        // wave_total is rewritten by the next step
     }
 }
 

@@ -144,6 +144,17 @@ __device__ __forceinline__ void group_totals(float (&v)[N])
     }
 }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// waits for every outstanding global load and store of the wave, which would
+// cancel loads issued ahead of the barrier on purpose; use this one where the
+// barrier protects LDS data alone.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Last segment p with seg[p] <= r (segments are [seg[p], seg[p+1])); the
 // result is always in [0, P-1], whatever the offsets hold.
 __device__ inline int32_t segment_of_row(const int64_t *__restrict__ seg, int32_t P, int64_t r)
