@@ -186,8 +186,10 @@ __global__ void k_catalogue_candidates(const hwsel_problem_t *__restrict__ probs
                                        hwsel_cands_out_t out)
 {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // the wave's first row (wave-uniform): one scalar search per wave
+    const int64_t r_first = (int64_t)blockIdx.x * blockDim.x + __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
     if (r >= R) return;
-    const int32_t p = segment_of_row(seg, P, r);
+    const int32_t p = segment_of_row_after(seg, P, r, r_first);
     int64_t i = point ? (int64_t)point[r] : r - seg[p];
     i = i < 0 ? 0 : (i >= kCat ? kCat - 1 : i);
     const Knobs k = decode(i);

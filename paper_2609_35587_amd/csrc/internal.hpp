@@ -167,4 +167,16 @@ __device__ inline int32_t segment_of_row(const int64_t *__restrict__ seg, int32_
     return lo;
 }
 
+// segment_of_row for the lanes of one wave, whose rows r are consecutive and
+// start at r_first (wave-uniform, r_first <= r): one search for r_first, on
+// the scalar unit, then each lane steps past the segments that end at or
+// before its row, usually none.  For non-decreasing offsets the result is
+// segment_of_row(seg, P, r); it is in [0, P-1] whatever the offsets hold.
+__device__ inline int32_t segment_of_row_after(const int64_t *__restrict__ seg, int32_t P, int64_t r, int64_t r_first)
+{
+    int32_t p = segment_of_row(seg, P, r_first);
+    while (p + 1 < P && seg[p + 1] <= r) ++p;
+    return p;
+}
+
 }  // namespace hwsel
