@@ -368,11 +368,22 @@ __global__ void k_static_accumulate(const float *__restrict__ rt, const int64_t 
     if (id >= n_cfg) return;
     int32_t c = 0;
     double s = 0.0;
-    for (int32_t p = 0; p < P; ++p) {
-        const int32_t j = first[(int64_t)p * n_cfg + id];
-        if (j == INT_MAX) continue;
-        ++c;
-        s += y_of(t_best[p], rt[seg[p] + j]);
+    // Eight problems at a time: their table entries, then their runtimes,
+    // are requested together; the sum still runs in problem order.
+    constexpr int kB = 8;
+    for (int32_t p0 = 0; p0 < P; p0 += kB) {
+        int32_t j[kB];
+#pragma unroll
+        for (int b = 0; b < kB; ++b) j[b] = p0 + b < P ? first[(int64_t)(p0 + b) * n_cfg + id] : INT_MAX;
+        float t[kB];
+#pragma unroll
+        for (int b = 0; b < kB; ++b) t[b] = j[b] != INT_MAX ? rt[seg[p0 + b] + j[b]] : 0.0f;
+#pragma unroll
+        for (int b = 0; b < kB; ++b)
+            if (j[b] != INT_MAX) {
+                ++c;
+                s += y_of(t_best[p0 + b], t[b]);
+            }
     }
     count[id] = c;
     ysum[id] = s;

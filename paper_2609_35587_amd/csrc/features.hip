@@ -316,8 +316,13 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
     for (int e = threadIdx.x; e < nf * kFbSlots; e += kFbThreads) u[(e >> 8) * kFbStride + (e & 255)] = U[e];
     __syncthreads();
     constexpr int kPass = F % 64 == 0 ? 64 : 32;      // columns per evaluation of the map
-    for (int64_t r = (int64_t)blockIdx.x * kFbThreads + threadIdx.x; r < R; r += (int64_t)gridDim.x * kFbThreads) {
-        const int32_t p = segment_of_row(seg, P, r);
+    // A wave's rows are consecutive: one scalar search for its first row,
+    // each lane steps forward from there.
+    const int wave_base = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
+    for (int64_t rw = (int64_t)blockIdx.x * kFbThreads + wave_base; rw < R; rw += (int64_t)gridDim.x * kFbThreads) {
+        const int64_t r = rw + (threadIdx.x & 63);
+        if (r >= R) break;
+        const int32_t p = segment_of_row_after(seg, P, r, rw);
         const hwsel_problem_t pb = probs[p];
         uint32_t word[F / 4];
 #pragma unroll
