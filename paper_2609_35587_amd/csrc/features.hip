@@ -283,8 +283,10 @@ __global__ __launch_bounds__(256) void k_sample_score(HwDev h, const hwsel_probl
                                                        float *__restrict__ scores)
 {
     const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    // the wave's first row (wave-uniform): one scalar search per wave
+    const int64_t r_first = (int64_t)blockIdx.x * 256 + __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
     if (r >= R) return;
-    const hwsel_problem_t pb = probs[segment_of_row(seg, P, r)];
+    const hwsel_problem_t pb = probs[segment_of_row_after(seg, P, r, r_first)];
     const int64_t M = max64(pb.M, 1), N = max64(pb.N, 1);
     const int64_t tm = max64(c.tile_m[r], 1), tn = max64(c.tile_n[r], 1), tk = max64(c.tile_k[r], 1);
     const int64_t st = max64(c.stages[r], 1);
