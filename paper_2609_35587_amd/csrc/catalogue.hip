@@ -3,10 +3,10 @@
 // Constraints", Table "Static validity constraints").
 //
 // A point index decodes to its knobs by mixed radix (first knob slowest), so
-// the mask pass never stores the catalogue: each thread decodes four
-// consecutive points and writes their four mask bytes as one word.  The
-// compaction is one workgroup per problem, an ordered block-wide scan over
-// the problem's mask.
+// the mask pass never stores the catalogue: each thread decodes one group of
+// 18 consecutive points (the three fastest knobs' combinations) once and
+// tests the 18; a block's mask bytes leave LDS as whole words.  The
+// compaction is one workgroup per problem, an ordered scan over its mask.
 #include "internal.hpp"
 
 namespace hwsel {
@@ -67,39 +67,53 @@ __global__ void k_zero_i64(int64_t *__restrict__ a, int32_t n)
 
 constexpr int kMaskThreads = 256;
 constexpr int64_t kWords = (kCat + 3) / 4;
+// The three fastest knobs (tile scheduler, epilogue, kernel schedule) take
+// 2 x 3 x 3 = 18 values; the 18 consecutive points of a group share every
+// other knob, decoded once.
+constexpr int kGroup = 18;
+constexpr int64_t kGroups = kCat / kGroup;
+static_assert(kCat % kGroup == 0 && kCat % 4 == 0, "catalogue groups");
+constexpr int kBlockBytes = kMaskThreads * kGroup;           // points (mask bytes) per block
 
 __global__ __launch_bounds__(kMaskThreads) void k_catalogue_mask(HwDev h, const hwsel_problem_t *__restrict__ probs,
                                                                  int32_t P, uint32_t flags, uint8_t *__restrict__ mask,
                                                                  int64_t *__restrict__ n_valid)
 {
-    __shared__ int32_t red[kMaskThreads];
+    __shared__ uint32_t stage[kBlockBytes / 4];
+    __shared__ int32_t wave_cnt[kMaskThreads / 64];
+    uint8_t *stage_b = reinterpret_cast<uint8_t *>(stage);
+    const int64_t g = (int64_t)blockIdx.x * kMaskThreads + threadIdx.x;   // this thread's group
+    const int64_t block_point0 = (int64_t)blockIdx.x * kBlockBytes;
+    const int block_bytes = (int)(kCat - block_point0 < kBlockBytes ? kCat - block_point0 : kBlockBytes);
     for (int32_t p = blockIdx.y; p < P; p += gridDim.y) {
-    const hwsel_problem_t pb = probs[p];
-    const int64_t w = (int64_t)blockIdx.x * kMaskThreads + threadIdx.x;
-    int32_t cnt = 0;
-    if (w < kWords) {
-        uint32_t word = 0;
+        const hwsel_problem_t pb = probs[p];
+        float cnt = 0.0f;
+        if (g < kGroups) {
+            Knobs k = decode(g * kGroup);                // the group's first point: fast knobs 0
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t i = 4 * w + q;
-            if (i < kCat && valid(h, pb, flags, decode(i))) {
-                word |= 1u << (8 * q);
-                ++cnt;
+            for (int j = 0; j < kGroup; ++j) {
+                k.ts = j % 2;
+                k.es = (j / 2) % 3;
+                k.ks = j / 6;
+                const bool ok = valid(h, pb, flags, k);
+                stage_b[threadIdx.x * kGroup + j] = ok ? 1 : 0;
+                cnt += ok ? 1.0f : 0.0f;
             }
         }
-        uint8_t *row = mask + (int64_t)p * kCat;
-        // kCat is a multiple of 4 and every row starts 4-byte aligned when mask is
-        *reinterpret_cast<uint32_t *>(row + 4 * w) = word;
-    }
-    red[threadIdx.x] = cnt;
-    __syncthreads();
-    for (int s = kMaskThreads / 2; s > 0; s >>= 1) {
-        if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        // per-wave totals (exact: at most 64 x 18 in fp32), then one LDS step
+        float tot[1] = {cnt};
+        group_totals<64, 1>(tot);
+        if ((threadIdx.x & 63) == 63) wave_cnt[threadIdx.x >> 6] = (int32_t)tot[0];
         __syncthreads();
-    }
-    if (threadIdx.x == 0 && red[0]) atomicAdd(reinterpret_cast<unsigned long long *>(n_valid + p),
-                                              (unsigned long long)red[0]);
-    __syncthreads();
+        uint32_t *row = reinterpret_cast<uint32_t *>(mask + (int64_t)p * kCat + block_point0);
+        for (int e = threadIdx.x; e < block_bytes / 4; e += kMaskThreads) row[e] = stage[e];
+        if (threadIdx.x == 0) {
+            int32_t t = 0;
+#pragma unroll
+            for (int i = 0; i < kMaskThreads / 64; ++i) t += wave_cnt[i];
+            if (t) atomicAdd(reinterpret_cast<unsigned long long *>(n_valid + p), (unsigned long long)t);
+        }
+        __syncthreads();                                 // stage and wave_cnt are reused for the next problem
     }
 }
 
@@ -215,7 +229,7 @@ hipError_t launch_catalogue_mask(const HwDev &h, const hwsel_problem_t *probs, i
                                  uint8_t *mask, int64_t *n_valid, hipStream_t s)
 {
     hipLaunchKernelGGL(k_zero_i64, dim3((P + 255) / 256), dim3(256), 0, s, n_valid, P);
-    const dim3 grid((unsigned)((kWords + kMaskThreads - 1) / kMaskThreads), (unsigned)(P < 65535 ? P : 65535));
+    const dim3 grid((unsigned)((kGroups + kMaskThreads - 1) / kMaskThreads), (unsigned)(P < 65535 ? P : 65535));
     hipLaunchKernelGGL(k_catalogue_mask, grid, dim3(kMaskThreads), 0, s, h, probs, P, flags, mask, n_valid);
     return hipGetLastError();
 }
