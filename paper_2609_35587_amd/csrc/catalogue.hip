@@ -117,15 +117,33 @@ __global__ __launch_bounds__(kMaskThreads) void k_catalogue_mask(HwDev h, const 
     }
 }
 
-__global__ void k_catalogue_offsets(const int64_t *__restrict__ n_valid, int32_t P, int64_t *__restrict__ seg)
+// seg[0] = 0, seg[p + 1] = seg[p] + max(n_valid[p], 0): one workgroup, each
+// thread summing a contiguous range of problems, the range sums scanned in
+// LDS (exact integer sums, so the order is free).
+constexpr int kOffsetThreads = 1024;
+
+__global__ __launch_bounds__(kOffsetThreads) void k_catalogue_offsets(const int64_t *__restrict__ n_valid, int32_t P,
+                                                                      int64_t *__restrict__ seg)
 {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        int64_t acc = 0;
-        seg[0] = 0;
-        for (int32_t p = 0; p < P; ++p) {
-            acc += n_valid[p] > 0 ? n_valid[p] : 0;
-            seg[p + 1] = acc;
-        }
+    __shared__ int64_t part[kOffsetThreads];
+    const int t = threadIdx.x;
+    const int64_t per = ((int64_t)P + kOffsetThreads - 1) / kOffsetThreads;
+    const int64_t lo = t * per < P ? t * per : P, hi = lo + per < P ? lo + per : P;
+    int64_t s = 0;
+    for (int64_t i = lo; i < hi; ++i) s += n_valid[i] > 0 ? n_valid[i] : 0;
+    part[t] = s;
+    __syncthreads();
+    for (int d = 1; d < kOffsetThreads; d <<= 1) {      // inclusive scan of the range sums
+        const int64_t v = t >= d ? part[t - d] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    int64_t acc = t > 0 ? part[t - 1] : 0;
+    if (t == 0) seg[0] = 0;
+    for (int64_t i = lo; i < hi; ++i) {
+        acc += n_valid[i] > 0 ? n_valid[i] : 0;
+        seg[i + 1] = acc;
     }
 }
 
@@ -237,7 +255,7 @@ hipError_t launch_catalogue_mask(const HwDev &h, const hwsel_problem_t *probs, i
 hipError_t launch_catalogue_compact(const uint8_t *mask, const int64_t *n_valid, int32_t P, int64_t *seg,
                                     int32_t *point, int64_t cap, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_catalogue_offsets, dim3(1), dim3(64), 0, s, n_valid, P, seg);
+    hipLaunchKernelGGL(k_catalogue_offsets, dim3(1), dim3(kOffsetThreads), 0, s, n_valid, P, seg);
     hipLaunchKernelGGL(k_catalogue_compact, dim3(P), dim3(kCompactThreads), 0, s, mask, seg, point, cap);
     return hipGetLastError();
 }
