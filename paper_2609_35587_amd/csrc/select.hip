@@ -5,7 +5,10 @@
 // every key unique: "score descending, index ascending" becomes "key
 // descending" and the answer is unique.  The k best keys are found by k
 // rounds of a block-wide maximum restricted to keys below the previous
-// winner; a segment is read k times, from L2 after the first round.
+// winner.  A segment of up to 8,192 rows is read once into registers (32
+// keys per thread); a longer one is read k times, from L2 after the first
+// round.  The wave maximum of a 64-bit key runs on DPP: the high words'
+// maximum, then the low words of the lanes that hold it.
 #include "internal.hpp"
 
 namespace hwsel {
@@ -51,6 +54,48 @@ __device__ __forceinline__ uint64_t wave_min(uint64_t v)
     return v;
 }
 
+template <int CTRL, int ROW_MASK, bool ZERO_FILL>
+__device__ __forceinline__ uint32_t dpp_max_u32(uint32_t v)
+{
+    const uint32_t w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xf, ZERO_FILL);
+    return w > v ? w : v;
+}
+
+// Maximum over the wave of an unsigned 32-bit value (0 is the identity), in
+// every lane: scan within rows, row broadcasts to lane 63, then readlane.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
+{
+    v = dpp_max_u32<0x111, 0xf, true>(v);
+    v = dpp_max_u32<0x112, 0xf, true>(v);
+    v = dpp_max_u32<0x114, 0xf, true>(v);
+    v = dpp_max_u32<0x118, 0xf, true>(v);
+    v = dpp_max_u32<0x142, 0xa, false>(v);
+    v = dpp_max_u32<0x143, 0xc, false>(v);
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Maximum over the wave of 64-bit keys: the largest high word, then the
+// largest low word among the lanes holding it.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t v)
+{
+    const uint32_t hi = wave_max_u32((uint32_t)(v >> 32));
+    const uint32_t lo = wave_max_u32((uint32_t)(v >> 32) == hi ? (uint32_t)v : 0u);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Block maximum with one barrier: the waves' maxima go to sh (a buffer the
+// caller alternates between rounds, so no round overwrites one still read).
+__device__ __forceinline__ uint64_t block_max_key(uint64_t v, uint64_t *sh)
+{
+    v = wave_max_key(v);
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint64_t r = sh[0];
+#pragma unroll
+    for (int w = 1; w < kThreads / 64; ++w) r = sh[w] > r ? sh[w] : r;
+    return r;
+}
+
 template <bool kMax>
 __device__ uint64_t block_reduce(uint64_t v, uint64_t *sh)
 {
@@ -72,23 +117,21 @@ __device__ __forceinline__ int64_t seg_len(const int64_t *seg, int32_t p)
     return n > 0x7fffffff ? 0x7fffffff : n;
 }
 
+constexpr int kRegRows = 32;      // keys per thread held in registers: segments up to 8,192 rows
+
 __global__ __launch_bounds__(kThreads) void k_topk(const float *__restrict__ scores,
                                                     const int64_t *__restrict__ seg, int32_t k,
                                                     int32_t *__restrict__ idx, float *__restrict__ vals)
 {
-    __shared__ uint64_t sh[kThreads / 64];
+    __shared__ uint64_t sh[2][kThreads / 64];
     const int32_t p = blockIdx.x;
     const int64_t base = seg[p];
     const int64_t n = seg_len(seg, p);
     const float *s = scores + base;
-    uint64_t prev = ~0ull;
-    for (int32_t j = 0; j < k; ++j) {
-        uint64_t best = 0;
-        for (int64_t i = threadIdx.x; i < n; i += kThreads) {
-            const uint64_t key = ((uint64_t)desc_bits(s[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
-            best = (key < prev && key > best) ? key : best;
-        }
-        best = block_reduce<true>(best, sh);
+    auto key_of = [&](int64_t i) {
+        return ((uint64_t)desc_bits(s[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
+    };
+    auto emit = [&](int32_t j, uint64_t best) {
         if (threadIdx.x == 0) {
             const int64_t o = (int64_t)p * k + j;
             if (best == 0) {
@@ -100,7 +143,34 @@ __global__ __launch_bounds__(kThreads) void k_topk(const float *__restrict__ sco
                 if (vals) vals[o] = s[li];
             }
         }
-        prev = best;
+    };
+    uint64_t prev = ~0ull;
+    if (n <= (int64_t)kThreads * kRegRows) {            // block-uniform
+        uint64_t key[kRegRows];
+#pragma unroll
+        for (int r = 0; r < kRegRows; ++r) {
+            const int64_t i = threadIdx.x + (int64_t)r * kThreads;
+            key[r] = i < n ? key_of(i) : 0ull;           // 0: no row (every real key is > 0)
+        }
+        for (int32_t j = 0; j < k; ++j) {
+            uint64_t best = 0;
+#pragma unroll
+            for (int r = 0; r < kRegRows; ++r) best = (key[r] < prev && key[r] > best) ? key[r] : best;
+            best = block_max_key(best, sh[j & 1]);
+            emit(j, best);
+            prev = best;
+        }
+    } else {
+        for (int32_t j = 0; j < k; ++j) {
+            uint64_t best = 0;
+            for (int64_t i = threadIdx.x; i < n; i += kThreads) {
+                const uint64_t key = key_of(i);
+                best = (key < prev && key > best) ? key : best;
+            }
+            best = block_max_key(best, sh[j & 1]);
+            emit(j, best);
+            prev = best;
+        }
     }
 }
 
