@@ -34,26 +34,6 @@ __device__ __forceinline__ uint32_t asc_bits(float t)
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
-__device__ __forceinline__ uint64_t wave_max(uint64_t v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t w = __shfl_xor(v, o, 64);
-        v = w > v ? w : v;
-    }
-    return v;
-}
-
-__device__ __forceinline__ uint64_t wave_min(uint64_t v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t w = __shfl_xor(v, o, 64);
-        v = w < v ? w : v;
-    }
-    return v;
-}
-
 template <int CTRL, int ROW_MASK, bool ZERO_FILL>
 __device__ __forceinline__ uint32_t dpp_max_u32(uint32_t v)
 {
@@ -93,20 +73,6 @@ __device__ __forceinline__ uint64_t block_max_key(uint64_t v, uint64_t *sh)
     uint64_t r = sh[0];
 #pragma unroll
     for (int w = 1; w < kThreads / 64; ++w) r = sh[w] > r ? sh[w] : r;
-    return r;
-}
-
-template <bool kMax>
-__device__ uint64_t block_reduce(uint64_t v, uint64_t *sh)
-{
-    v = kMax ? wave_max(v) : wave_min(v);
-    const int wave = threadIdx.x >> 6;
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) sh[wave] = v;
-    __syncthreads();
-    uint64_t r = sh[0];
-#pragma unroll
-    for (int w = 1; w < kThreads / 64; ++w) r = kMax ? (sh[w] > r ? sh[w] : r) : (sh[w] < r ? sh[w] : r);
     return r;
 }
 
@@ -196,7 +162,7 @@ __global__ __launch_bounds__(kThreads) void k_regret(const float *__restrict__ r
         const uint64_t key = ((uint64_t)asc_bits(t[i]) << 32) | (uint64_t)(uint32_t)i;
         m = key < m ? key : m;
     }
-    m = block_reduce<false>(m, sh);
+    m = ~block_max_key(~m, sh);                         // block minimum of the unique keys
     if (threadIdx.x != 0) return;
     if (n == 0) {
         r1[p] = __builtin_nanf("");
