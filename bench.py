@@ -171,7 +171,7 @@ def main():
                          "reference for the HBM byte counters)")
     a = ap.parse_args()
     if a.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {a.gpus}); "
+        print(f"bench.py: measures one GPU only (asked for --gpus {a.gpus}); "
               "the path shards by problem segment across GPUs, which is not built here.", file=sys.stderr)
         sys.exit(2)
 

@@ -37,7 +37,7 @@ extern "C" {
 typedef enum {
     HWSEL_OK = 0,
     HWSEL_EINVAL = 1,       /* a null pointer, a size out of range, misalignment */
-    HWSEL_EUNSUPPORTED = 2, /* a valid request this build does not implement */
+    HWSEL_EUNSUPPORTED = 2, /* a valid request the library does not implement */
     HWSEL_EHIP = 3          /* the HIP runtime reported an error at launch */
 } hwsel_status;
 
