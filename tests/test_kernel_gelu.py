@@ -100,3 +100,16 @@ def test_bf16_roundings_move_only_near_a_boundary():
     assert np.all(step <= 1e-6 + np.abs(exact[moved]) * 2.0 ** -7)
     large = np.abs(exact) > 0.1
     assert moved[large].mean() < 1e-3, float(moved[large].mean())
+
+
+def test_coefficients_come_from_the_committed_fit():
+    """The kernel's coefficients are what csrc/gelu_fit.py produces (fp32),
+    and the fit's own error check gives the bound the source states."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("gelu_fit", SRC.parent / "gelu_fit.py")
+    fit = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(fit)
+    c = fit.fit()
+    assert [np.float32(v) for v in c] == coefficients()
+    err, _ = fit.max_error(c)
+    assert err <= 6e-7
