@@ -241,6 +241,69 @@ __global__ void k_catalogue_candidates(const hwsel_problem_t *__restrict__ probs
     out.tile_sched[r] = (uint8_t)k.ts;
 }
 
+// Four consecutive rows per thread, each field written with one 4-byte
+// (8-bit fields) or 8-byte (16-bit fields) store; taken when every field
+// array is aligned for that (the rows of a partial last quad are stored one
+// by one).
+__global__ void k_catalogue_candidates4(const hwsel_problem_t *__restrict__ probs, int32_t P,
+                                        const int64_t *__restrict__ seg, const int32_t *__restrict__ point,
+                                        int64_t R, hwsel_cands_out_t out)
+{
+    const int64_t r0 = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+    const int64_t r_first = 4 * ((int64_t)blockIdx.x * blockDim.x + __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u));
+    if (r0 >= R) return;
+    int32_t p = segment_of_row_after(seg, P, r0, r_first);
+    uint32_t tm[4], tn[4], tk[4], st[4], cm[4], cn[4], ik[4], ks[4], es[4], ts[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t r = r0 + j < R ? r0 + j : R - 1;
+        while (p + 1 < P && seg[p + 1] <= r) ++p;
+        int64_t i = point ? (int64_t)point[r] : r - seg[p];
+        i = i < 0 ? 0 : (i >= kCat ? kCat - 1 : i);
+        const Knobs k = decode(i);
+        const int dt = probs[p].dtype < 2 ? probs[p].dtype : 2;
+        tm[j] = (uint32_t)k.tm; tn[j] = (uint32_t)k.tn; tk[j] = (uint32_t)k.tk; st[j] = (uint32_t)k.st;
+        cm[j] = (uint32_t)k.cm; cn[j] = (uint32_t)k.cn; ik[j] = dt == 2 ? 32u : 16u;
+        ks[j] = (uint32_t)k.ks; es[j] = (uint32_t)k.es; ts[j] = (uint32_t)k.ts;
+    }
+    if (r0 + 3 < R) {
+        auto p16 = [](const uint32_t (&v)[4]) {
+            return make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+        };
+        auto p8 = [](const uint32_t (&v)[4]) { return v[0] | (v[1] << 8) | (v[2] << 16) | (v[3] << 24); };
+        *reinterpret_cast<uint2 *>(out.tile_m + r0) = p16(tm);
+        *reinterpret_cast<uint2 *>(out.tile_n + r0) = p16(tn);
+        *reinterpret_cast<uint2 *>(out.tile_k + r0) = p16(tk);
+        *reinterpret_cast<uint2 *>(out.inst_n + r0) = p16(tn);
+        *reinterpret_cast<uint32_t *>(out.stages + r0) = p8(st);
+        *reinterpret_cast<uint32_t *>(out.cluster_m + r0) = p8(cm);
+        *reinterpret_cast<uint32_t *>(out.cluster_n + r0) = p8(cn);
+        *reinterpret_cast<uint32_t *>(out.swizzle + r0) = 0x01010101u;
+        *reinterpret_cast<uint32_t *>(out.inst_m_div16 + r0) = 0x04040404u;
+        *reinterpret_cast<uint32_t *>(out.inst_k + r0) = p8(ik);
+        *reinterpret_cast<uint32_t *>(out.kernel_sched + r0) = p8(ks);
+        *reinterpret_cast<uint32_t *>(out.epi_sched + r0) = p8(es);
+        *reinterpret_cast<uint32_t *>(out.tile_sched + r0) = p8(ts);
+    } else {
+        for (int j = 0; j < 4 && r0 + j < R; ++j) {
+            const int64_t r = r0 + j;
+            out.tile_m[r] = (uint16_t)tm[j];
+            out.tile_n[r] = (uint16_t)tn[j];
+            out.tile_k[r] = (uint16_t)tk[j];
+            out.inst_n[r] = (uint16_t)tn[j];
+            out.stages[r] = (uint8_t)st[j];
+            out.cluster_m[r] = (uint8_t)cm[j];
+            out.cluster_n[r] = (uint8_t)cn[j];
+            out.swizzle[r] = 1;
+            out.inst_m_div16[r] = 4;
+            out.inst_k[r] = (uint8_t)ik[j];
+            out.kernel_sched[r] = (uint8_t)ks[j];
+            out.epi_sched[r] = (uint8_t)es[j];
+            out.tile_sched[r] = (uint8_t)ts[j];
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_catalogue_mask(const HwDev &h, const hwsel_problem_t *probs, int32_t P, uint32_t flags,
@@ -263,8 +326,19 @@ hipError_t launch_catalogue_compact(const uint8_t *mask, const int64_t *n_valid,
 hipError_t launch_catalogue_candidates(const hwsel_problem_t *probs, int32_t P, const int64_t *seg,
                                        const int32_t *point, int64_t R, const hwsel_cands_out_t &out, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_catalogue_candidates, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, probs, P, seg,
-                       point, R, out);
+    auto al = [](const void *q, uintptr_t a) { return ((uintptr_t)q & (a - 1)) == 0; };
+    const bool packed = al(out.tile_m, 8) && al(out.tile_n, 8) && al(out.tile_k, 8) && al(out.inst_n, 8) &&
+                        al(out.stages, 4) && al(out.cluster_m, 4) && al(out.cluster_n, 4) && al(out.swizzle, 4) &&
+                        al(out.inst_m_div16, 4) && al(out.inst_k, 4) && al(out.kernel_sched, 4) &&
+                        al(out.epi_sched, 4) && al(out.tile_sched, 4);
+    if (packed) {
+        const int64_t quads = (R + 3) / 4;
+        hipLaunchKernelGGL(k_catalogue_candidates4, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, probs, P,
+                           seg, point, R, out);
+    } else {
+        hipLaunchKernelGGL(k_catalogue_candidates, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, probs, P,
+                           seg, point, R, out);
+    }
     return hipGetLastError();
 }
 

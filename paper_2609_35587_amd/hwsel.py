@@ -425,12 +425,14 @@ def hwsel_catalogue_compact(mask: torch.Tensor, n_valid: torch.Tensor, capacity:
 
 
 def hwsel_catalogue_candidates(problems: torch.Tensor, seg_offsets: torch.Tensor, R: int,
-                               point: torch.Tensor | None = None, stream=None) -> dict:
-    """Candidate SoA (name -> device tensor of length R) of catalogue points."""
+                               point: torch.Tensor | None = None, out: dict | None = None, stream=None) -> dict:
+    """Candidate SoA (name -> device tensor of length R) of catalogue points;
+    ``out`` may supply the field tensors (allocated here if None)."""
     P = problems.shape[0]
     dev = problems.device
     wide = ("tile_m", "tile_n", "tile_k", "inst_n")
-    out = {n: torch.empty(R, dtype=torch.int16 if n in wide else torch.uint8, device=dev) for n in CAND_FIELDS}
+    if out is None:
+        out = {n: torch.empty(R, dtype=torch.int16 if n in wide else torch.uint8, device=dev) for n in CAND_FIELDS}
     s = hwsel_cands_out_t(*[_ptr(out[n]) for n in CAND_FIELDS])
     _check("hwsel_catalogue_candidates", lib().hwsel_catalogue_candidates(
         _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")), _ptr(point), R, C.byref(s),

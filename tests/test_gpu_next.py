@@ -292,3 +292,25 @@ def test_evaluate_many_problems():
     rt = rng.choice(np.array([1.0, 1.25, 1.5, 2.0, 4.0, np.inf], np.float32), R)
     idx, _ = oracle.topk(rng.standard_normal(R).astype(np.float32), seg, 1)
     eval_compare(rt, seg, idx)
+
+
+def test_catalogue_rows_any_field_alignment():
+    """Field arrays offset by one element (so no packed stores apply) give
+    the oracle's rows too, with a row count that is not a multiple of four
+    and segments that end inside a group of four rows."""
+    say("catalogue rows, misaligned fields")
+    pr = catalogue_problems()[[0, 2, 5]]
+    seg = np.array([0, 1001, 2003, 2010], np.int64)
+    R = int(seg[-1])
+    wide = ("tile_m", "tile_n", "tile_k", "inst_n")
+    bufs = {n: torch.zeros(R + 1, dtype=torch.int16 if n in wide else torch.uint8, device="cuda")
+            for n in hwsel.CAND_FIELDS}
+    prd = up(pr)
+    for off in (0, 1):
+        out = {n: t[off:off + R] for n, t in bufs.items()}
+        c = hwsel.hwsel_catalogue_candidates(prd, up(seg), R, out=out)
+        for p in range(len(pr)):
+            ref = oracle.catalogue_decode(np.arange(seg[p + 1] - seg[p]), int(pr["dtype"][p]))
+            for n in hwsel.CAND_FIELDS:
+                got = c[n].cpu().numpy()[seg[p]:seg[p + 1]]
+                assert np.array_equal(got.view(ref[n].dtype), ref[n]), (off, p, n)
