@@ -433,6 +433,10 @@ def hwsel_catalogue_candidates(problems: torch.Tensor, seg_offsets: torch.Tensor
     wide = ("tile_m", "tile_n", "tile_k", "inst_n")
     if out is None:
         out = {n: torch.empty(R, dtype=torch.int16 if n in wide else torch.uint8, device=dev) for n in CAND_FIELDS}
+    for n in CAND_FIELDS:
+        t = _dev(out[n], n)
+        if t.element_size() != (2 if n in wide else 1) or t.numel() < R:
+            raise ValueError(f"{n} must hold at least R elements of {2 if n in wide else 1} byte(s)")
     s = hwsel_cands_out_t(*[_ptr(out[n]) for n in CAND_FIELDS])
     _check("hwsel_catalogue_candidates", lib().hwsel_catalogue_candidates(
         _ptr(_dev(problems, "problems")), P, _ptr(_dev(seg_offsets, "seg_offsets")), _ptr(point), R, C.byref(s),

@@ -174,6 +174,12 @@ def test_catalogue_rejects(L):
     assert L.hwsel_catalogue_candidates(FAKE, 4, FAKE, None, 10, C.byref(out), None) == 1
     out = hwsel.hwsel_cands_out_t(*([FAKE] * 13))
     assert L.hwsel_catalogue_candidates(FAKE, 4, FAKE, None, 0, C.byref(out), None) == 1
+    # the binding refuses caller-supplied rows that are not device arrays
+    import torch
+    cpu = {n: torch.zeros(8, dtype=torch.uint8) for n in hwsel.CAND_FIELDS}
+    with pytest.raises(ValueError):
+        hwsel.hwsel_catalogue_candidates(torch.zeros(1, 16, dtype=torch.uint8), torch.zeros(2, dtype=torch.int64), 8,
+                                         out=cpu)
 
 
 def test_fused_selection_rejects(L):
