@@ -210,3 +210,18 @@ def test_fused_selection_rejects(L):
     deep = hwsel.forest_struct(dict(f, depth=11))
     assert call(f=deep) == 2
     assert L.hwsel_last_error().startswith(b"hwsel_select_forest: ")
+
+
+def test_missing_library_fails_loudly():
+    """Without libhwsel.so every entry point raises; nothing falls back to
+    another implementation."""
+    code = ("from paper_2609_35587_amd import hwsel\n"
+            "hwsel.LIB_PATH = '/nonexistent/libhwsel.so'\n"
+            "try:\n"
+            "    hwsel.lib()\n"
+            "except RuntimeError as e:\n"
+            "    assert 'no CPU fallback' in str(e), e\n"
+            "    print('raised')\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run(["python", "-c", code], capture_output=True, text=True, cwd=root, timeout=120)
+    assert out.returncode == 0 and out.stdout.strip() == "raised", out.stderr
