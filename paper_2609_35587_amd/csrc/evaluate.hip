@@ -244,81 +244,170 @@ __global__ void k_eval_aggregate(const double *__restrict__ regret, const int32_
 }
 
 // Up to kSmallP problems: one workgroup stages the per-problem values in LDS,
-// sorts the counted regrets with a bitonic network, and takes the sums in
-// problem order from LDS; the same outputs as k_eval_select +
-// k_eval_aggregate.
+// sorts the counted regrets with a bitonic network held in registers (element
+// tid + 1024 m in thread tid; partners less than 64 apart are exchanged
+// inside the wave, the others through LDS or within the thread), counts in
+// parallel and takes the two sums in problem order from LDS; the same
+// outputs as k_eval_select + k_eval_aggregate.
 constexpr int kSmallP = 4096;
+constexpr int kSmallT = 1024, kSmallM = kSmallP / kSmallT;
 
-__global__ __launch_bounds__(1024) void k_eval_small(const double *__restrict__ regret,
-                                                     const int32_t *__restrict__ rank,
-                                                     const double *__restrict__ ybar, int32_t P,
-                                                     double *__restrict__ out, double *__restrict__ regret_out,
-                                                     int32_t *__restrict__ rank_out, double *__restrict__ ybar_out)
+// Lane l's double as a wave-uniform value.
+__device__ __forceinline__ double bcast_lane(double v, int l)
+{
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, l), hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), l);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// One compare-exchange of the network as seen from element i, which holds
+// `own` and whose partner (index i ^ j) holds `other`: the lower index keeps
+// the smaller value when the block of size k runs upwards.
+__device__ __forceinline__ double bitonic_keep(double own, double other, int32_t i, int32_t j, int32_t k)
+{
+    const bool up = (i & k) == 0;
+    const bool lower = (i & j) == 0;
+    const double a = lower ? own : other, b = lower ? other : own;   // a at the lower index
+    const bool swap = (a > b) == up;
+    return lower ? (swap ? b : a) : (swap ? a : b);
+}
+
+__global__ __launch_bounds__(kSmallT) void k_eval_small(const double *__restrict__ regret,
+                                                        const int32_t *__restrict__ rank,
+                                                        const double *__restrict__ ybar, int32_t P,
+                                                        double *__restrict__ out, double *__restrict__ regret_out,
+                                                        int32_t *__restrict__ rank_out, double *__restrict__ ybar_out)
 {
     __shared__ double reg_s[kSmallP], yb_s[kSmallP], sorted[kSmallP];
     __shared__ int32_t rank_s[kSmallP];
-    for (int32_t i = threadIdx.x; i < kSmallP; i += 1024) {
-        const bool in = i < P;
-        reg_s[i] = in ? regret[i] : 0.0;
-        yb_s[i] = in ? ybar[i] : 0.0;
-        rank_s[i] = in ? rank[i] : 0;
-        sorted[i] = (in && rank[i] != 0) ? regret[i] : __builtin_inf();   // uncounted sort last
-    }
-    __syncthreads();
-    int32_t n2 = 1;
+    __shared__ double wmax[kSmallT / 64];
+    __shared__ int64_t wcnt[4][kSmallT / 64];
+    const int32_t tid = threadIdx.x;
+    int32_t n2 = 2;
     while (n2 < P) n2 <<= 1;
+    const int32_t mcount = (n2 + kSmallT - 1) / kSmallT;      // register slots in use (uniform)
+    double v[kSmallM];
+    int64_t cnt = 0, top1 = 0, top5 = 0, w5 = 0;
+    double mx = -__builtin_inf();
+#pragma unroll
+    for (int m = 0; m < kSmallM; ++m) {
+        const int32_t i = tid + kSmallT * m;
+        const bool in = i < P;
+        const double r = in ? regret[i] : 0.0;
+        const int32_t rk = in ? rank[i] : 0;
+        reg_s[i] = r;
+        yb_s[i] = in ? ybar[i] : 0.0;
+        rank_s[i] = rk;
+        const bool c = rk != 0;
+        v[m] = c ? r : __builtin_inf();                          // uncounted sort last
+        cnt += c;
+        top1 += c && rk == 1;
+        top5 += c && rk <= 5;
+        w5 += c && r <= 0.05;
+        mx = (c && r > mx) ? r : mx;
+    }
     for (int32_t k = 2; k <= n2; k <<= 1)
         for (int32_t j = k >> 1; j > 0; j >>= 1) {
-            for (int32_t i = threadIdx.x; i < n2; i += 1024) {
-                const int32_t l = i ^ j;
-                if (l > i) {
-                    const double a = sorted[i], b = sorted[l];
-                    const bool up = (i & k) == 0;
-                    if ((a > b) == up) {
-                        sorted[i] = b;
-                        sorted[l] = a;
-                    }
+            if (j >= kSmallT) {                                     // partner in the same thread
+                static_assert(kSmallM == 4, "slot pairs below");
+                auto cx = [&](double &lo, double &hi, int m) {
+                    const bool swap = (lo > hi) == (((tid + kSmallT * m) & k) == 0);
+                    const double a = lo, b = hi;
+                    lo = swap ? b : a;
+                    hi = swap ? a : b;
+                };
+                if (j == kSmallT) {                                 // slots m and m + 1
+                    cx(v[0], v[1], 0);
+                    if (mcount > 2) cx(v[2], v[3], 2);
+                } else {                                            // slots m and m + 2
+                    cx(v[0], v[2], 0);
+                    cx(v[1], v[3], 1);
                 }
+            } else if (j >= 64) {                                   // partner in another wave
+#pragma unroll
+                for (int m = 0; m < kSmallM; ++m)
+                    if (m < mcount) sorted[tid + kSmallT * m] = v[m];
+                __syncthreads();
+#pragma unroll
+                for (int m = 0; m < kSmallM; ++m)
+                    if (m < mcount) {
+                        const int32_t i = tid + kSmallT * m;
+                        v[m] = bitonic_keep(v[m], sorted[i ^ j], i, j, k);
+                    }
+                __syncthreads();
+            } else {                                                // partner in the same wave
+#pragma unroll
+                for (int m = 0; m < kSmallM; ++m)
+                    if (m < mcount) {
+                        const int32_t i = tid + kSmallT * m;
+                        v[m] = bitonic_keep(v[m], __shfl_xor(v[m], j), i, j, k);
+                    }
             }
-            __syncthreads();
         }
-    if (threadIdx.x == 0) {
-        int64_t cnt = 0, top1 = 0, top5 = 0, w5 = 0;
-        double sum = 0.0, rsum = 0.0, mx = -__builtin_inf();
-        // Branch-free so the LDS reads pipeline: adding +0.0 for an
-        // uncounted problem leaves a sum that starts at +0.0 unchanged.
-#pragma unroll 8
-        for (int32_t p = 0; p < P; ++p) {
-            const int32_t rk = rank_s[p];
-            const bool c = rk != 0;
-            const double r = reg_s[p];
-            cnt += c;
-            sum += c ? r : 0.0;
-            rsum += c ? 1.0 - yb_s[p] : 0.0;
-            mx = (c && r > mx) ? r : mx;
-            top1 += c && rk == 1;
-            top5 += c && rk <= 5;
-            w5 += c && r <= 0.05;
+#pragma unroll
+    for (int m = 0; m < kSmallM; ++m)
+        if (m < mcount) sorted[tid + kSmallT * m] = v[m];
+    // counts and the maximum: wave totals, then the waves in order (integer
+    // sums and a maximum do not depend on the order)
+    for (int off = 32; off > 0; off >>= 1) {
+        cnt += __shfl_xor(cnt, off);
+        top1 += __shfl_xor(top1, off);
+        top5 += __shfl_xor(top5, off);
+        w5 += __shfl_xor(w5, off);
+        const double o = __shfl_xor(mx, off);
+        mx = o > mx ? o : mx;
+    }
+    if ((tid & 63) == 0) {
+        const int w = tid >> 6;
+        wcnt[0][w] = cnt; wcnt[1][w] = top1; wcnt[2][w] = top5; wcnt[3][w] = w5;
+        wmax[w] = mx;
+    }
+    __syncthreads();
+    if (tid < 64) {
+        // the sums in problem order: wave 0 loads 64 problems at a time and
+        // adds them one by one from lane values broadcast as scalars (adding
+        // +0.0 for an uncounted problem leaves a sum that starts at +0.0
+        // unchanged)
+        double sum = 0.0, rsum = 0.0;
+        for (int32_t base = 0; base < P; base += 64) {
+            const int32_t p = base + tid < P ? base + tid : P - 1;   // lanes past P read problem P - 1
+            const bool c = base + tid < P && rank_s[p] != 0;
+            const double r = c ? reg_s[p] : 0.0;
+            const double y = c ? 1.0 - yb_s[p] : 0.0;
+            const int n = P - base < 64 ? P - base : 64;
+            for (int l = 0; l < n; ++l) {
+                sum += bcast_lane(r, l);
+                rsum += bcast_lane(y, l);
+            }
         }
-        if (cnt == 0) {
-            for (int i = 0; i < 8; ++i) out[i] = __builtin_nan("");
-            out[8] = 0.0;
-        } else {
-            const double p50 = 0.5 * (double)(cnt - 1), p95 = 0.95 * (double)(cnt - 1);
-            const int64_t l50 = (int64_t)__builtin_floor(p50), l95 = (int64_t)__builtin_floor(p95);
-            const int64_t h50 = l50 + 1 < cnt ? l50 + 1 : cnt - 1, h95 = l95 + 1 < cnt ? l95 + 1 : cnt - 1;
-            out[0] = sum / (double)cnt;
-            out[1] = interpolate(sorted[l50], sorted[h50], cnt, 0.5);
-            out[2] = interpolate(sorted[l95], sorted[h95], cnt, 0.95);
-            out[3] = mx;
-            out[4] = (double)top1 / (double)cnt;
-            out[5] = (double)top5 / (double)cnt;
-            out[6] = (double)w5 / (double)cnt;
-            out[7] = rsum / (double)cnt;
-            out[8] = (double)cnt;
+        cnt = top1 = top5 = w5 = 0;
+        mx = -__builtin_inf();
+#pragma unroll 1
+        for (int w = 0; w < kSmallT / 64; ++w) {
+            cnt += wcnt[0][w]; top1 += wcnt[1][w]; top5 += wcnt[2][w]; w5 += wcnt[3][w];
+            mx = wmax[w] > mx ? wmax[w] : mx;
+        }
+        if (tid == 0) {
+            if (cnt == 0) {
+                for (int i = 0; i < 8; ++i) out[i] = __builtin_nan("");
+                out[8] = 0.0;
+            } else {
+                const double p50 = 0.5 * (double)(cnt - 1), p95 = 0.95 * (double)(cnt - 1);
+                const int64_t l50 = (int64_t)__builtin_floor(p50), l95 = (int64_t)__builtin_floor(p95);
+                const int64_t h50 = l50 + 1 < cnt ? l50 + 1 : cnt - 1, h95 = l95 + 1 < cnt ? l95 + 1 : cnt - 1;
+                out[0] = sum / (double)cnt;
+                out[1] = interpolate(sorted[l50], sorted[h50], cnt, 0.5);
+                out[2] = interpolate(sorted[l95], sorted[h95], cnt, 0.95);
+                out[3] = mx;
+                out[4] = (double)top1 / (double)cnt;
+                out[5] = (double)top5 / (double)cnt;
+                out[6] = (double)w5 / (double)cnt;
+                out[7] = rsum / (double)cnt;
+                out[8] = (double)cnt;
+            }
         }
     }
-    for (int32_t p = threadIdx.x; p < P; p += 1024) {
+    for (int32_t p = tid; p < P; p += kSmallT) {
         if (regret_out) regret_out[p] = reg_s[p];
         if (rank_out) rank_out[p] = rank_s[p];
         if (ybar_out) ybar_out[p] = yb_s[p];
