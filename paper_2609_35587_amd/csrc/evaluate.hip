@@ -247,8 +247,8 @@ __global__ void k_eval_aggregate(const double *__restrict__ regret, const int32_
 // sorts the counted regrets with a bitonic network held in registers (element
 // tid + 1024 m in thread tid; partners less than 64 apart are exchanged
 // inside the wave, the others through LDS or within the thread), counts in
-// parallel and takes the two sums in problem order from LDS; the same
-// outputs as k_eval_select + k_eval_aggregate.
+// parallel, and wave 0 takes the two sums in problem order; the same outputs
+// as k_eval_select + k_eval_aggregate.
 constexpr int kSmallP = 4096;
 constexpr int kSmallT = 1024, kSmallM = kSmallP / kSmallT;
 
@@ -534,7 +534,7 @@ hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const
     int32_t *rank = reinterpret_cast<int32_t *>(w + 3 * up256((size_t)P * 8));
     hipLaunchKernelGGL(k_eval_groups, dim3(P), dim3(kEvalThreads), 0, s, rt, seg, P, idx, k, regret, rank, ybar);
     if (P <= kSmallP) {
-        hipLaunchKernelGGL(k_eval_small, dim3(1), dim3(1024), 0, s, regret, rank, ybar, P, out, regret_out, rank_out,
+        hipLaunchKernelGGL(k_eval_small, dim3(1), dim3(kSmallT), 0, s, regret, rank, ybar, P, out, regret_out, rank_out,
                            ybar_out);
     } else {
         hipLaunchKernelGGL(k_eval_select, dim3(1), dim3(kSelectThreads), 0, s, regret, rank, P, stats);
