@@ -457,9 +457,10 @@ __global__ void k_static_accumulate(const float *__restrict__ rt, const int64_t 
     if (id >= n_cfg) return;
     int32_t c = 0;
     double s = 0.0;
-    // Eight problems at a time: their table entries, then their runtimes,
-    // are requested together; the sum still runs in problem order.
-    constexpr int kB = 8;
+    // 32 problems at a time: their table entries, then their runtimes, are
+    // requested together (one wave per SIMD: the loads in flight are what
+    // hides the memory latency); the sum still runs in problem order.
+    constexpr int kB = 32;
     for (int32_t p0 = 0; p0 < P; p0 += kB) {
         int32_t j[kB];
 #pragma unroll
