@@ -428,10 +428,13 @@ __global__ void k_static_first(const int64_t *__restrict__ seg, int32_t P, const
                                int32_t n_cfg, int32_t *__restrict__ first)
 {
     const int64_t R = seg[P];
-    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < R; r += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    // the wave's first row (wave-uniform): one scalar search per wave
+    int64_t r_first = (int64_t)blockIdx.x * blockDim.x + __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < R; r += stride, r_first += stride) {
+        const int32_t p = segment_of_row_after(seg, P, r, r_first);
         const int32_t id = cfg[r];
         if (id < 0 || id >= n_cfg) continue;
-        const int32_t p = segment_of_row(seg, P, r);
         if (r < seg[p] || r >= seg[p + 1]) continue;
         atomicMin(&first[(int64_t)p * n_cfg + id], (int32_t)(r - seg[p]));
     }
