@@ -129,6 +129,7 @@ def test_topk_regret_edge_cases(k):
     s[rng.random(R) < 0.01] = np.inf
     rt = np.exp(rng.standard_normal(R)).astype(np.float32)
     rt[rng.random(R) < 0.03] = np.inf
+    rt[rng.random(R) < 0.03] = np.nan      # never finishing: a NaN pick has regret 1
     rt[rng.random(R) < 0.2] = 1.0          # many equal runtimes
     sd, segd, rtd = (torch.from_numpy(a).cuda() for a in (s, seg, rt))
     idx, vals = hwsel.hwsel_topk_per_problem(sd, segd, k)

@@ -252,3 +252,50 @@ def test_feature_tiers_are_prefixes():
     full = feat(1000, 2000, 3000, F=128)
     for F in (64, 96):
         assert np.array_equal(feat(1000, 2000, 3000, F=F), full[:F])
+
+
+# ----------------------------------------------------------------------------
+# Hand-derived values of the columns no enumeration or identity above reaches
+# ----------------------------------------------------------------------------
+def _hand_cases():
+    cases, order = {}, []
+    for raw in open(os.path.join(GOLDEN, "hand_features.txt")):
+        line = raw.split("#")[0].split()
+        if not line:
+            continue
+        if line[0] == "case":
+            name = line[1]
+            M, N, K, lay, dt = map(int, line[2:7])
+            assert line[7] == "|"
+            tm, tn, tk, st, cm, cn, swz, im, in_, ik, ks, es, ts = map(int, line[8:21])
+            cases[name] = dict(args=dict(M=M, N=N, K=K, layout=lay, dtype=dt, tile_m=tm, tile_n=tn, tile_k=tk,
+                                         stages=st, cluster_m=cm, cluster_n=cn, swizzle=swz, inst_m_div16=im // 16,
+                                         inst_n=in_, inst_k=ik, kernel_sched=ks, epi_sched=es, tile_sched=ts),
+                               cols=[])
+            order.append(name)
+        else:
+            cases[line[0]]["cols"].append((int(line[1]), line[2:]))
+    return [(n, cases[n]) for n in order]
+
+
+@pytest.mark.parametrize("name,case", _hand_cases(), ids=[n for n, _ in _hand_cases()])
+def test_hand_derived_columns(name, case):
+    """Columns 21, 26-28, 40-41, 46-47, 50-51, 55, 81, 90-91, 101-124 against
+    values worked out by hand from the paper's definitions
+    (tests/golden/hand_features.txt): an exact ratio must match bit for bit
+    (one binary64 division rounded to fp32), a short binary64 sequence within
+    1e-6 relative."""
+    x = feat(**case["args"])
+    assert len(case["cols"]) >= 30
+    for col, spec in case["cols"]:
+        if spec[0] == "sqrt":
+            want = np.float32(math.sqrt(int(spec[1])))
+            assert x[col] == want, (name, col, x[col], want)
+        elif spec[0] == "q":
+            num, den = map(int, spec[1].split("/"))
+            want = num / den
+            assert abs(float(x[col]) - want) <= 1e-6 * abs(want), (name, col, x[col], want)
+        else:
+            num, den = map(int, spec[0].split("/"))
+            want = np.float32(float(num) / float(den))
+            assert x[col] == want, (name, col, x[col], want)

@@ -85,3 +85,24 @@ def test_regret_edge_cases():
     rt2 = np.array([1.0, np.inf], np.float32)
     r1, _, _ = oracle.regret(rt2, np.array([0, 2], np.int64), np.array([[1]], np.int32))
     assert r1[0] == 1.0
+
+
+def test_nan_pick_reads_as_never_finishing():
+    """One reading of eq. (regret) for a pick whose runtime is NaN: a kernel
+    that never finishes has throughput 0, so R = 1 - 0 / T* = 1 -- in the
+    regret call and in the evaluation metrics alike, also when every runtime
+    of the group is NaN (no candidate finishes, none is matched)."""
+    rt = np.array([1.0, np.nan, 2.0, np.nan, np.nan, 0.5, np.nan], np.float32)
+    seg = np.array([0, 3, 5, 7], np.int64)
+    idx = np.array([[1, 0], [0, 1], [1, 0]], np.int32)
+    r1, rk, best = oracle.regret(rt, seg, idx)
+    assert r1.tolist() == [1.0, 1.0, 1.0]
+    # best of the two picks: {NaN, 1.0} -> 1.0 = t*; {NaN, NaN} -> 1; {NaN, 0.5} -> 0.5 = t*
+    assert rk.tolist() == [0.0, 1.0, 0.0]
+    assert best.tolist() == [0, 0, 0]
+    _, reg, _, _ = oracle.evaluate(rt, seg, idx[:, :1])
+    assert reg.tolist() == r1.astype(np.float64).tolist()
+    # a NaN pick next to a finite best equals the regret of an infinitely slow pick
+    inf_pick = oracle.regret(np.array([1.0, np.inf], np.float32), np.array([0, 2], np.int64),
+                             np.array([[1]], np.int32))[0]
+    assert inf_pick[0] == 1.0
