@@ -243,8 +243,10 @@ int hwsel_topk_per_problem(const float *scores, const int64_t *seg_offsets, int3
  *   regret_top1[p]  = 1 - t_best / t(idx[p][0])          (binary64, then fp32),
  *   regret_bestk[p] = 1 - t_best / min_j t(idx[p][j])    (nullable),
  *   best_idx[p]     = local index of t_best, lowest on ties (nullable).
- * Equal runtimes (inf included) give exactly 0; NaN runtimes rank above +inf;
- * an empty segment or a -1 pick gives NaN and best_idx -1.
+ * Equal runtimes (inf included) give exactly 0; NaN runtimes rank above +inf
+ * and a pick whose runtime is NaN (a kernel that never finishes, T = 0) gives
+ * exactly 1, as in hwsel_evaluate; an empty segment or a -1 pick gives NaN,
+ * and an empty segment best_idx -1.
  *   runtimes [R] fp32 (seconds), idx int32 [P][k] as from
  *   hwsel_topk_per_problem (entries outside [-1, segment length) are read as
  *   -1).
@@ -324,7 +326,7 @@ int hwsel_sample_score(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t P
  * Selection metrics over problems (section "Selection Regret (The Target
  * Metric)") and the uniform-random baseline (section "Final Fit and Test
  * Protocol").  With y(p,c) = t_best / t_c (1 when t_c == t_best, 0 for a NaN
- * runtime, read as never finishing, unless every runtime is NaN), for each
+ * runtime, read as never finishing, also when every runtime is NaN), for each
  * problem p whose segment is non-empty and whose pick c_hat = idx[p][0] is a
  * valid local index ("counted" problems):
  *   regret[p] = 1 - y(p, c_hat)                       binary64

@@ -540,7 +540,9 @@ int oracle_topk(const float *scores, const int64_t *seg, int64_t P, int32_t k, i
 /* T(c_hat) / T_star = t_star / t(c_hat).  R1 uses the top-1 pick, Rk the    */
 /* best of the top-k picks.  best = argmin runtime, lowest index on ties (local index).  */
 /* Readings: NaN runtimes rank above +inf; equal runtimes (also inf == inf)  */
-/* give R = 0 exactly; an empty segment gives NaN regrets and best = -1.     */
+/* give R = 0 exactly; a pick whose runtime is NaN is a kernel that never    */
+/* finishes (T = 0), so R = 1 (also when every runtime is NaN); an empty     */
+/* segment or a -1 pick gives NaN regrets, and an empty one best = -1.       */
 /* Parity: pinned by R >= 0, Rk <= R1, R1 = 0 when scores = -runtimes, and   */
 /* the expected regret of a uniform pick.                                    */
 /* ------------------------------------------------------------------------ */
@@ -555,6 +557,7 @@ static int faster(float a, int32_t ia, float b, int32_t ib)
 static float regret_of(float t_star, float t_sel)
 {
     if (t_sel == t_star) return 0.0f;
+    if (isnan(t_sel)) return 1.0f;
     return (float)(1.0 - (double)t_star / (double)t_sel);
 }
 
@@ -678,7 +681,7 @@ int oracle_linear(const o_linear *m, const float *X, int64_t ld, int64_t n, floa
 /*              0 when equal; 1 for a NaN runtime, read as never finishing), */
 /*   rank     = 1 + #{c : t_c faster than t(c_hat)}  (minimum-rank ties),   */
 /*   ybar(g)  = mean_c y(g,c), y = 1 when t_c == t_best, 0 when t_c is NaN  */
-/*              (and t_best is not), else t_best / t_c; random-pick regret  */
+/*              (never finishing), else t_best / t_c; random-pick regret    */
 /*              1 - ybar.                                                   */
 /* A group counts when its segment is non-empty and c_hat is a valid local  */
 /* index.  Aggregates over counted groups, binary64, group order:           */

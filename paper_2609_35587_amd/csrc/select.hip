@@ -140,9 +140,12 @@ __global__ __launch_bounds__(kThreads) void k_topk(const float *__restrict__ sco
     }
 }
 
+// 1 - t_star / t_pick in binary64; equal runtimes (inf included) give 0 and a
+// NaN runtime (a kernel that never finishes) gives 1.
 __device__ __forceinline__ float regret_value(float t_star, float t_pick)
 {
     if (t_pick == t_star) return 0.0f;
+    if (t_pick != t_pick) return 1.0f;
     return (float)(1.0 - (double)t_star / (double)t_pick);
 }
 
