@@ -70,10 +70,12 @@ __device__ __forceinline__ float gelu_fast(float a)
     p = fmaf(p, x, c2);
     p = fmaf(p, x, c1);
     p = fmaf(p, x, c0);
-    // max(a, 0) without the NaN-quieting copy the compiler adds to fmaxf
-    // (a is a finite accumulator here)
-    float pos;
-    asm("v_max_f32_e32 %0, 0, %1" : "=v"(pos) : "v"(a));
+    // max(a, 0) as a signed-integer maximum of the bit pattern: exact for
+    // every non-NaN a (a negative float, -0 included, has a negative pattern),
+    // one instruction without the NaN-quieting copy fmaxf adds, and visible to
+    // the compiler, which must see this first read of an accumulator to place
+    // the wait states the matrix core needs before it
+    const float pos = __int_as_float(max(__float_as_int(a), 0));
     return fmaf(-x, __builtin_amdgcn_exp2f(p), pos);
 }
 
@@ -195,16 +197,6 @@ __device__ __forceinline__ int act_offset(int row, int row_bytes, int unit)
     return row * row_bytes + ((((unit >> 3) ^ row) & 15) | ((unit >> 3) & ~15)) * 16 + (unit & 7) * 2;
 }
 
-// Between a block's last products and the first vector instruction reading
-// their results: a scheduling barrier and 32 wait states, so that no read of
-// an accumulator can be placed before the matrix core has written it.
-__device__ __forceinline__ void products_done()
-{
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
-    __builtin_amdgcn_sched_barrier(0);
-}
-
 // acc[mt][nt] = init[mt] + products of the wave's two consecutive M-tiles
 // (fragments at W0 and W0 + KS fragments) with 4 N-tiles: every activation
 // fragment read serves two products and every weight fragment four.  The
@@ -252,7 +244,6 @@ __device__ __forceinline__ void mma_block_mt2_direct(const bf16x8 *__restrict__ 
 #pragma unroll
         for (int j = 0; j < PF; ++j) step(j, ks + j, false);
     }
-    products_done();
 }
 
 // acc[nt] = init + products of one M-tile (fragments at W) with the 4
@@ -288,7 +279,6 @@ __device__ __forceinline__ void mma_block_mt1_direct(const bf16x8 *__restrict__ 
 #pragma unroll
         for (int j = 0; j < PF; ++j) step(j, ks + j, false);
     }
-    products_done();
 }
 
 // Bias of one 32-unit M-tile starting at unit u0, in accumulator layout.
