@@ -11,7 +11,8 @@
  * Conventions for every entry point
  *   - Array arguments are DEVICE pointers (memory of the current HIP device)
  *     unless the comment says "host".  The caller owns every buffer; the
- *     library allocates nothing, frees nothing and keeps no device state.
+ *     library allocates nothing, frees nothing and keeps no device state
+ *     (one exception: the scratch array of hwsel_evaluate_noalloc).
  *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
  *     Calls only enqueue work on it: they return before the work finishes and
  *     never synchronise.
@@ -354,6 +355,28 @@ int hwsel_evaluate_workspace_bytes(int32_t P, size_t *bytes);
 int hwsel_evaluate(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx, int32_t k,
                    double *out, double *regret, int32_t *rank, double *ybar, void *workspace,
                    size_t workspace_bytes, void *stream);
+
+/*
+ * hwsel_evaluate for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops and harnesses that forbid hipMalloc): no
+ * workspace argument, and no allocation of any kind.  The same kernels
+ * compute the same outputs, bit for bit, as hwsel_evaluate; the per-problem
+ * intermediates live in a device array of the library's code object
+ * (HWSEL_EVAL_NOALLOC_SCRATCH_BYTES = 1,835,008 bytes per device, held until
+ * the process ends), whose address is looked up once per device, on the
+ * first call made with that device current.  All calls on one device share
+ * that array: calls that overlap on one device (streams or threads without
+ * an order between them) race and their results are undefined.  Nothing
+ * carries over from one call to the next.
+ *   Arguments as for hwsel_evaluate; P <= HWSEL_EVAL_NOALLOC_MAX_P.
+ * Returns HWSEL_EINVAL as hwsel_evaluate does and for P >
+ * HWSEL_EVAL_NOALLOC_MAX_P; HWSEL_EHIP when the array's address cannot be
+ * looked up or a launch fails.
+ */
+#define HWSEL_EVAL_NOALLOC_MAX_P 65536
+#define HWSEL_EVAL_NOALLOC_SCRATCH_BYTES 1835008
+int hwsel_evaluate_noalloc(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx,
+                           int32_t k, double *out, double *regret, int32_t *rank, double *ybar, void *stream);
 
 /*
  * Best static configuration (baseline of section "Final Fit and Test

@@ -149,6 +149,25 @@ int hwsel_evaluate(const float *runtimes, const int64_t *seg_offsets, int32_t P,
                     fn);
 }
 
+int hwsel_evaluate_noalloc(const float *runtimes, const int64_t *seg_offsets, int32_t P, const int32_t *idx,
+                           int32_t k, double *out, double *regret, int32_t *rank, double *ybar, void *stream)
+{
+    static const char *fn = "hwsel_evaluate_noalloc";
+    if (!runtimes || !seg_offsets || !idx || !out) return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (P < 1 || P > HWSEL_EVAL_NOALLOC_MAX_P)
+        return fail(HWSEL_EINVAL, fn, "P=%d (1..%d)", P, HWSEL_EVAL_NOALLOC_MAX_P);
+    if (k < 1 || k > 64) return fail(HWSEL_EINVAL, fn, "k=%d (1..64)", k);
+    void *scratch = nullptr;
+    size_t scratch_bytes = 0;
+    const hipError_t e = hwsel::evaluate_noalloc_scratch(&scratch, &scratch_bytes);
+    if (e != hipSuccess) return fail(HWSEL_EHIP, fn, "scratch address: %s", hipGetErrorString(e));
+    if (scratch_bytes < hwsel::evaluate_workspace_bytes(P) || scratch_bytes != HWSEL_EVAL_NOALLOC_SCRATCH_BYTES)
+        return fail(HWSEL_EHIP, fn, "scratch of %zu bytes", scratch_bytes);
+    return launched(hwsel::launch_evaluate(runtimes, seg_offsets, P, idx, k, out, regret, rank, ybar, scratch,
+                                           (hipStream_t)stream),
+                    fn);
+}
+
 int hwsel_static_config_workspace_bytes(int32_t P, int32_t n_configs, size_t *bytes)
 {
     static const char *fn = "hwsel_static_config_workspace_bytes";

@@ -6,6 +6,8 @@
 // over at most a few hundred thousand problems.
 #include <limits.h>
 
+#include <mutex>
+
 #include "internal.hpp"
 
 namespace hwsel {
@@ -520,11 +522,48 @@ __global__ __launch_bounds__(1024) void k_static_argmax(const int32_t *__restric
 
 size_t up256(size_t v) { return (v + 255) / 256 * 256; }
 
+constexpr size_t eval_workspace_bytes(int64_t P)
+{
+    return 3 * (((size_t)P * sizeof(double) + 255) / 256 * 256) + ((size_t)P * sizeof(int32_t) + 255) / 256 * 256;
+}
+
+// Scratch of hwsel_evaluate_noalloc: the per-problem regrets, y means, order
+// statistics and ranks that hwsel_evaluate keeps in the caller's workspace,
+// here in a device array of the library's code object (one copy per device,
+// held until the process ends).  Every value a call reads is written earlier
+// in that same call, so nothing has to be cleared between calls; calls that
+// overlap on one device share the array and race.
+constexpr size_t kNoAllocScratchBytes = eval_workspace_bytes(HWSEL_EVAL_NOALLOC_MAX_P);
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+static_assert(kNoAllocScratchBytes == HWSEL_EVAL_NOALLOC_SCRATCH_BYTES, "scratch size as declared");
+
 }  // namespace
 
-size_t evaluate_workspace_bytes(int32_t P)
+size_t evaluate_workspace_bytes(int32_t P) { return eval_workspace_bytes(P); }
+
+// Device address of this device's scratch copy, looked up (with the device
+// current) on the first call on each device and kept.  In host code the
+// array's own name is not a device address and is never passed to a kernel.
+hipError_t evaluate_noalloc_scratch(void **ptr, size_t *bytes)
 {
-    return 3 * up256((size_t)P * sizeof(double)) + up256((size_t)P * sizeof(int32_t));
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void *per_device[kMaxDevices];
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!per_device[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        per_device[dev] = p;
+    }
+    *ptr = per_device[dev];
+    *bytes = kNoAllocScratchBytes;
+    return hipSuccess;
 }
 
 hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx, int32_t k,

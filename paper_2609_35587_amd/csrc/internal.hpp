@@ -35,6 +35,9 @@ hipError_t launch_linear(const hwsel_linear_t &lin, const float *X, int64_t R, i
                          hipStream_t s);
 
 size_t evaluate_workspace_bytes(int32_t P);
+// Device address and size of this device's scratch array of the
+// allocation-free evaluation (see evaluate.hip).
+hipError_t evaluate_noalloc_scratch(void **ptr, size_t *bytes);
 hipError_t launch_evaluate(const float *rt, const int64_t *seg, int32_t P, const int32_t *idx, int32_t k,
                            double *out, double *regret_out, int32_t *rank_out, double *ybar_out, void *ws,
                            hipStream_t s);

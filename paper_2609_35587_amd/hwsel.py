@@ -96,6 +96,7 @@ def lib() -> C.CDLL:
                                           C.POINTER(hwsel_forest_t), vp, i32, vp, vp, vp, vp, sz, vp]
         L.hwsel_evaluate_workspace_bytes.argtypes = [i32, C.POINTER(sz)]
         L.hwsel_evaluate.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.hwsel_evaluate_noalloc.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp]
         L.hwsel_static_config_workspace_bytes.argtypes = [i32, i32, C.POINTER(sz)]
         L.hwsel_static_config.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, sz, vp]
         L.hwsel_catalogue_mask.argtypes = [hwsel_hw_t, vp, i32, C.c_uint32, vp, vp, vp]
@@ -376,6 +377,29 @@ def hwsel_evaluate(runtimes: torch.Tensor, seg_offsets: torch.Tensor, idx: torch
         _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P, _ptr(_dev(idx, "idx")), k,
         _ptr(out), _ptr(reg), _ptr(rank), _ptr(ybar), _ptr(workspace), workspace.numel(), _stream(stream)))
     return out, reg, rank, ybar
+
+
+HWSEL_EVAL_NOALLOC_MAX_P = 65536
+
+
+def hwsel_evaluate_noalloc(runtimes: torch.Tensor, seg_offsets: torch.Tensor, idx: torch.Tensor,
+                           out: torch.Tensor | None = None, regret: torch.Tensor | None = None,
+                           rank: torch.Tensor | None = None, ybar: torch.Tensor | None = None,
+                           per_group: bool = True, stream=None):
+    """hwsel_evaluate without a workspace (the library's own scratch array);
+    outputs as for hwsel_evaluate.  Output tensors may be passed in."""
+    P, k = idx.shape
+    dev = runtimes.device
+    if out is None:
+        out = torch.empty(HWSEL_EVAL_FIELDS, dtype=torch.float64, device=dev)
+    if per_group:
+        regret = torch.empty(P, dtype=torch.float64, device=dev) if regret is None else regret
+        rank = torch.empty(P, dtype=torch.int32, device=dev) if rank is None else rank
+        ybar = torch.empty(P, dtype=torch.float64, device=dev) if ybar is None else ybar
+    _check("hwsel_evaluate_noalloc", lib().hwsel_evaluate_noalloc(
+        _ptr(_dev(runtimes, "runtimes")), _ptr(_dev(seg_offsets, "seg_offsets")), P, _ptr(_dev(idx, "idx")), k,
+        _ptr(out), _ptr(regret), _ptr(rank), _ptr(ybar), _stream(stream)))
+    return out, regret, rank, ybar
 
 
 def hwsel_static_config(runtimes: torch.Tensor, seg_offsets: torch.Tensor, config_id: torch.Tensor,

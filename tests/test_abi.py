@@ -162,6 +162,22 @@ def test_evaluation_rejects(L):
     assert L.hwsel_static_config(FAKE, FAKE, 600, FAKE, 65536, FAKE, FAKE, FAKE + 8, n.value, None) == 1
 
 
+def test_evaluation_noalloc_rejects(L):
+    # every rejection happens on the host, before the scratch array is looked up
+    max_p = hwsel.HWSEL_EVAL_NOALLOC_MAX_P
+    assert L.hwsel_evaluate_noalloc(FAKE, FAKE, max_p + 1, FAKE, 10, FAKE, None, None, None, None) == 1
+    assert b"P=65537" in L.hwsel_last_error()
+    assert L.hwsel_evaluate_noalloc(FAKE, FAKE, 0, FAKE, 10, FAKE, None, None, None, None) == 1
+    assert L.hwsel_evaluate_noalloc(FAKE, FAKE, 600, FAKE, 0, FAKE, None, None, None, None) == 1
+    assert L.hwsel_evaluate_noalloc(FAKE, FAKE, 600, FAKE, 65, FAKE, None, None, None, None) == 1
+    assert L.hwsel_evaluate_noalloc(None, FAKE, 600, FAKE, 10, FAKE, None, None, None, None) == 1
+    assert L.hwsel_evaluate_noalloc(FAKE, FAKE, 600, FAKE, 10, None, None, None, None, None) == 1
+    assert L.hwsel_last_error().startswith(b"hwsel_evaluate_noalloc: ")
+    # the declared scratch size holds the largest admitted workspace
+    n = C.c_size_t(0)
+    assert L.hwsel_evaluate_workspace_bytes(max_p, C.byref(n)) == 0 and n.value == 1835008
+
+
 def test_catalogue_rejects(L):
     assert L.hwsel_catalogue_mask(_hw(), FAKE, 0, 0, FAKE, FAKE, None) == 1
     assert L.hwsel_catalogue_mask(_hw(), FAKE, 4, 0, FAKE + 2, FAKE, None) == 1
