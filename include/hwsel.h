@@ -161,7 +161,9 @@ int hwsel_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *byt
  * same inputs give bit-identical scores from run to run).
  *   X: fp32 [R][ld], ld >= n_features, as written by hwsel_features.
  *   packed: NULL for the direct tree walk, or the image hwsel_forest_pack
- *     wrote for this very forest; then `workspace` must hold
+ *     wrote for this very forest (an image of another shape gives NaN
+ *     scores; one of the same shape but other values is not detected); then
+ *     `workspace` must hold
  *     hwsel_forest_workspace_bytes(f, R) bytes (device, 256-byte aligned).
  * Returns HWSEL_EINVAL for null pointers, R < 1, n_trees < 1, ld <
  * n_features, a short or misaligned workspace; HWSEL_EUNSUPPORTED for depth
@@ -170,6 +172,28 @@ int hwsel_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *byt
  */
 int hwsel_forest_score(const hwsel_forest_t *f, const void *packed, const float *X, int64_t R, int64_t ld,
                        float *scores, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * hwsel_forest_score (packed path only) with check outputs of the same
+ * traversal kernels: the scores are bit-identical to hwsel_forest_score's.
+ *   leaf_hash  uint64 [R] (nullable, 8-byte aligned): each row's leaf-path
+ *              fingerprint, the wrapping 64-bit sum over trees t of
+ *              mix(t * 2^32 + leaf_t), with leaf_t the index in [0, 2^depth)
+ *              of the leaf the row reaches in tree t and mix the 64-bit
+ *              finaliser of SplitMix64 (Steele, Lea, Flood, OOPSLA 2014).
+ *              One changed leaf always changes it; tree order does not.
+ *   leaf_idx   uint16 [leaf_rows][n_trees] (nullable): leaf_idx[i][t] =
+ *              leaf_t of row leaf_row0 + i, for rows [leaf_row0, leaf_row0 +
+ *              leaf_rows) within [0, R).
+ * For a packed image whose stored shape (trees, depth, features, chunking)
+ * differs from the forest's, every score is NaN and nothing else is written
+ * (hwsel_forest_score does the same).
+ * Returns the status codes of hwsel_forest_score, and HWSEL_EINVAL for a
+ * NULL packed image, a misaligned leaf_hash or a row range outside [0, R).
+ */
+int hwsel_forest_score_checked(const hwsel_forest_t *f, const void *packed, const float *X, int64_t R, int64_t ld,
+                               float *scores, void *workspace, size_t workspace_bytes, uint64_t *leaf_hash,
+                               uint16_t *leaf_idx, int64_t leaf_row0, int64_t leaf_rows, void *stream);
 
 /*
  * Leaf index of every tree for selected rows: leaf_idx[i][t] = index in

@@ -135,8 +135,11 @@ def _forest_struct(f: dict, keep: list) -> _Forest:
     return s
 
 
-def forest(f: dict, X: np.ndarray, rows: np.ndarray | None = None, leaves: bool = False):
-    """Scores (and optionally leaf indices [n][T]) of rows of X."""
+def forest(f: dict, X: np.ndarray, rows: np.ndarray | None = None, leaves: bool = False,
+           leaf_hash: bool = False):
+    """Scores of rows of X; with ``leaves`` also the leaf indices [n][T], with
+    ``leaf_hash`` also each row's leaf-path fingerprint (uint64 [n]).  Returns
+    the scores alone, or a tuple (scores, leaves?, hashes?) of what was asked."""
     X = _c(X, np.float32)
     keep = []
     s = _forest_struct(f, keep)
@@ -145,8 +148,18 @@ def forest(f: dict, X: np.ndarray, rows: np.ndarray | None = None, leaves: bool 
     n = X.shape[0] if rows is None else len(rows)
     out = np.empty(n, np.float32)
     li = np.empty((n, s.n_trees), np.uint16) if leaves else None
-    lib().oracle_forest(C.byref(s), _p(X), C.c_int64(X.shape[1]), _p(rows), C.c_int64(n), _p(out), _p(li))
-    return (out, li) if leaves else out
+    lh = np.empty(n, np.uint64) if leaf_hash else None
+    lib().oracle_forest(C.byref(s), _p(X), C.c_int64(X.shape[1]), _p(rows), C.c_int64(n), _p(out), _p(li),
+                        _p(lh))
+    extra = tuple(a for a in (li, lh) if a is not None)
+    return (out, *extra) if extra else out
+
+
+def leaf_mix(z: int) -> int:
+    """The 64-bit mixer of the leaf-path fingerprint."""
+    lib().oracle_leaf_mix.restype = C.c_uint64
+    lib().oracle_leaf_mix.argtypes = [C.c_uint64]
+    return int(lib().oracle_leaf_mix(z))
 
 
 def forest_linked(f: dict, X: np.ndarray) -> np.ndarray:

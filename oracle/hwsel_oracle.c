@@ -307,8 +307,23 @@ typedef struct {
     const float *leaf_value;       /* [n_trees][2^depth] */
 } o_forest;
 
+/* Leaf-path fingerprint of a row (a check value, not part of the method):
+ * the wrapping 64-bit sum over trees t of mix(t * 2^32 + leaf_t), with mix
+ * the 64-bit finaliser of SplitMix64 (Steele, Lea and Flood, "Fast
+ * splittable pseudorandom number generators", OOPSLA 2014).  mix is a
+ * bijection, so one changed leaf always changes the sum; the sum does not
+ * depend on the order the trees are visited in. */
+static uint64_t leaf_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+uint64_t oracle_leaf_mix(uint64_t z) { return leaf_mix(z); }
+
 int oracle_forest(const o_forest *f, const float *X, int64_t ld, const int64_t *rows, int64_t n,
-                  float *scores, uint16_t *leaf_idx)
+                  float *scores, uint16_t *leaf_idx, uint64_t *leaf_hash)
 {
     const int64_t n_int = ((int64_t)1 << f->depth) - 1;
     const int64_t n_leaf = n_int + 1;
@@ -317,6 +332,7 @@ int oracle_forest(const o_forest *f, const float *X, int64_t ld, const int64_t *
     for (int64_t i = 0; i < n; ++i) {
         const float *x = X + (rows ? rows[i] : i) * ld;
         double acc = (double)f->base_score;
+        uint64_t hash = 0;
         for (int32_t t = 0; t < f->n_trees; ++t) {
             const uint8_t *feat = f->node_feature + t * n_int;
             const float *thr = f->node_threshold + t * n_int;
@@ -328,9 +344,11 @@ int oracle_forest(const o_forest *f, const float *X, int64_t ld, const int64_t *
             }
             const int64_t leaf = node - n_int;
             if (leaf_idx) leaf_idx[i * f->n_trees + t] = (uint16_t)leaf;
+            hash += leaf_mix(((uint64_t)t << 32) | (uint64_t)leaf);
             acc += (double)f->leaf_value[t * n_leaf + leaf];
         }
         scores[i] = (float)acc;
+        if (leaf_hash) leaf_hash[i] = hash;
     }
     return 0;
 }

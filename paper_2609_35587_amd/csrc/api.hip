@@ -305,6 +305,28 @@ int hwsel_forest_score(const hwsel_forest_t *f, const void *packed, const float 
     return launched(hwsel::launch_forest_packed(*f, packed, X, R, ld, scores, workspace, (hipStream_t)stream), fn);
 }
 
+int hwsel_forest_score_checked(const hwsel_forest_t *f, const void *packed, const float *X, int64_t R, int64_t ld,
+                               float *scores, void *workspace, size_t workspace_bytes, uint64_t *leaf_hash,
+                               uint16_t *leaf_idx, int64_t leaf_row0, int64_t leaf_rows, void *stream)
+{
+    static const char *fn = "hwsel_forest_score_checked";
+    if (int s = check_forest(f, X, R, ld, fn)) return s;
+    if (!scores || !packed) return fail(HWSEL_EINVAL, fn, "null scores or packed image");
+    if (!hwsel::packable(*f)) return fail(HWSEL_EUNSUPPORTED, fn, "forest shape cannot be packed");
+    if (!aligned16(packed)) return fail(HWSEL_EINVAL, fn, "packed not 16-byte aligned");
+    const size_t need = hwsel::packed_workspace_bytes(*f, R);
+    if (!workspace || workspace_bytes < need)
+        return fail(HWSEL_EINVAL, fn, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0) return fail(HWSEL_EINVAL, fn, "workspace not 256-byte aligned");
+    if (((uintptr_t)leaf_hash & 7u) != 0) return fail(HWSEL_EINVAL, fn, "leaf_hash not 8-byte aligned");
+    if (leaf_idx && (leaf_row0 < 0 || leaf_rows < 1 || leaf_row0 > R - leaf_rows))
+        return fail(HWSEL_EINVAL, fn, "leaf rows [%lld, %lld + %lld) outside [0, %lld)", (long long)leaf_row0,
+                    (long long)leaf_row0, (long long)leaf_rows, (long long)R);
+    return launched(hwsel::launch_forest_checked(*f, packed, X, R, ld, scores, workspace, leaf_hash, leaf_idx,
+                                                 leaf_row0, leaf_rows, (hipStream_t)stream),
+                    fn);
+}
+
 int hwsel_forest_leaves(const hwsel_forest_t *f, const float *X, int64_t R, int64_t ld, const int64_t *rows,
                         int64_t n_rows, uint16_t *leaf_idx, void *stream)
 {
@@ -353,7 +375,7 @@ int hwsel_select_forest(hwsel_hw_t hw, const hwsel_problem_t *problems, int32_t 
     hipStream_t s = (hipStream_t)stream;
     float *sc = scores ? scores : reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + base);
     hipError_t e = hwsel::launch_features_bins(h, problems, P, seg_offsets, c, R, n_features,
-                                               hwsel::packed_thresholds(packed), f->n_features,
+                                               packed, hwsel::packed_image_id(*f), f->n_features,
                                                hwsel::packed_nan_bin(*f), static_cast<uint8_t *>(workspace),
                                                hwsel::packed_bin_stride(*f), s);
     if (e == hipSuccess) e = hwsel::launch_forest_from_bins(*f, packed, R, sc, workspace, s);

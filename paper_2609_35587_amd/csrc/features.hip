@@ -310,10 +310,13 @@ constexpr int kFbChains = 8;
 template <int F>
 __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const hwsel_problem_t *__restrict__ probs,
                                                                  int32_t P, const int64_t *__restrict__ seg,
-                                                                 CandsDev c, int64_t R, const float *__restrict__ U,
-                                                                 int nf, uint32_t nan_bin, uint8_t *__restrict__ Xb,
+                                                                 CandsDev c, int64_t R,
+                                                                 const void *__restrict__ packed, ImageId id, int nf,
+                                                                 uint32_t nan_bin, uint8_t *__restrict__ Xb,
                                                                  int stride)
 {
+    if (!image_matches(packed, id)) return;
+    const float *__restrict__ U = reinterpret_cast<const float *>(static_cast<const uint8_t *>(packed) + 256);
     __shared__ float u[128 * kFbStride];
     for (int e = threadIdx.x; e < nf * kFbSlots; e += kFbThreads) u[(e >> 8) * kFbStride + (e & 255)] = U[e];
     __syncthreads();
@@ -372,8 +375,8 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
 }  // namespace
 
 hipError_t launch_features_bins(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
-                                const CandsDev &c, int64_t R, int32_t F, const float *U, int nf, uint32_t nan_bin,
-                                uint8_t *Xb, int stride, hipStream_t s)
+                                const CandsDev &c, int64_t R, int32_t F, const void *packed, ImageId id, int nf,
+                                uint32_t nan_bin, uint8_t *Xb, int stride, hipStream_t s)
 {
     int dev = 0, n_cu = 256;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -382,14 +385,14 @@ hipError_t launch_features_bins(const HwDev &hw, const hwsel_problem_t *problems
     const int64_t need = (R + kFbThreads - 1) / kFbThreads;
     const unsigned blocks = (unsigned)(need < n_cu ? need : n_cu);
     if (F == 64)
-        hipLaunchKernelGGL(k_features_bins<64>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R, U,
-                           nf, nan_bin, Xb, stride);
+        hipLaunchKernelGGL(k_features_bins<64>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R, packed,
+                           id, nf, nan_bin, Xb, stride);
     else if (F == 96)
-        hipLaunchKernelGGL(k_features_bins<96>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R, U,
-                           nf, nan_bin, Xb, stride);
+        hipLaunchKernelGGL(k_features_bins<96>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R, packed,
+                           id, nf, nan_bin, Xb, stride);
     else
         hipLaunchKernelGGL(k_features_bins<128>, dim3(blocks), dim3(kFbThreads), 0, s, hw, problems, P, seg, c, R,
-                           U, nf, nan_bin, Xb, stride);
+                           packed, id, nf, nan_bin, Xb, stride);
     return hipGetLastError();
 }
 

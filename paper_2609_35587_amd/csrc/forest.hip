@@ -172,13 +172,58 @@ PackGeom geometry(const hwsel_forest_t &f)
 
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 
+constexpr int32_t kImageMagic = 0x48575346;   // "FSWH"
+constexpr int32_t kImageVersion = 2;
+
+ImageId image_id(const hwsel_forest_t &f, const PackGeom &g)
+{
+    return ImageId{kImageMagic, kImageVersion, f.n_trees, f.depth, f.n_features, g.tc, g.n_chunks};
+}
+
+// Check outputs of the packed traversal (hwsel_forest_score_checked).
+struct LeafHook {
+    uint64_t *hash;          // [R] or null: leaf-path fingerprint per row
+    uint16_t *idx;           // [n_rows][n_trees] or null: leaf indices of rows [row0, row0 + n_rows)
+    int64_t row0, n_rows;
+    int32_t n_trees;
+};
+
+// 64-bit finaliser of SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): a
+// bijection, so the fingerprint sum changes whenever one leaf does.
+__device__ __forceinline__ uint64_t leaf_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+// Wrapping sum of a 64-bit value over the TC consecutive lanes of a group.
+template <int TC>
+__device__ __forceinline__ uint64_t group_sum_u64(uint64_t h)
+{
+#pragma unroll
+    for (int o = 1; o < TC; o <<= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)h, o, 64), hi = __shfl_xor((uint32_t)(h >> 32), o, 64);
+        h += ((uint64_t)hi << 32) | lo;
+    }
+    return h;
+}
+
+__global__ void k_fill_u64(uint64_t *__restrict__ a, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        a[i] = 0;
+}
+
 // ---------------------------------------------------------------------------
 // Packed path: kernels
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBinThreads, 1) void k_bin(const float *__restrict__ X, int64_t R, int64_t ld,
-                                                         const float *__restrict__ U, int nf, uint32_t nan_bin,
-                                                         uint8_t *__restrict__ Xb, int stride)
+                                                         const void *__restrict__ packed, ImageId id, int nf,
+                                                         uint32_t nan_bin, uint8_t *__restrict__ Xb, int stride)
 {
+    if (!image_matches(packed, id)) return;
+    const float *__restrict__ U = reinterpret_cast<const float *>(static_cast<const uint8_t *>(packed) + 256);
     // thresholds as order-preserving keys; index i of feature f at
     // bin_table_index(f, i), so each searched feature stays on its own bank
     __shared__ uint32_t u[128 * kBinSlots];
@@ -291,12 +336,15 @@ __device__ __forceinline__ void descend_root(int &node, uint32_t &code, uint32_t
 
 
 
-template <int TC, int D>
-__global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__restrict__ chunks, int n_chunks,
+template <int TC, int D, bool HOOK>
+__global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const void *__restrict__ packed, ImageId id,
+                                                              const uint8_t *__restrict__ chunks, int n_chunks,
                                                               const uint8_t *__restrict__ Xb, int64_t R,
                                                               int stride, int groups_per_xcd,
-                                                              int64_t rows_per_group, float *__restrict__ partial)
+                                                              int64_t rows_per_group, float *__restrict__ partial,
+                                                              LeafHook hook)
 {
+    if (!image_matches(packed, id)) return;
     constexpr int NS = 1 << D;
     constexpr int NODE_B = NS * TC * 2 * node_copies(TC);
     constexpr int CHUNK_B = NODE_B + NS * TC * 4;
@@ -436,6 +484,21 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
                         else descend_pair(node[a], code[a], bin[a], pair[a]);
                     }
                 }
+                if constexpr (HOOK) {
+#pragma unroll
+                    for (int a = 0; a < ILP; ++a) {
+                        const int64_t row = w0 + (it * ILP + a) * RPI + s;
+                        const int32_t tree = c * TC + t;
+                        const uint32_t leaf = (uint32_t)(node[a] - NS);
+                        const bool real = row < r_end && tree < hook.n_trees;   // padding trees count for nothing
+                        const uint64_t h =
+                            group_sum_u64<TC>(real ? leaf_mix(((uint64_t)tree << 32) | leaf) : 0ull);
+                        if (hook.hash && t == 0 && row < r_end)
+                            atomicAdd(reinterpret_cast<unsigned long long *>(hook.hash + row), (unsigned long long)h);
+                        if (hook.idx && real && row >= hook.row0 && row < hook.row0 + hook.n_rows)
+                            hook.idx[(row - hook.row0) * hook.n_trees + tree] = (uint16_t)leaf;
+                    }
+                }
                 // Leaves of all groups first, then the sums, then the stores
                 // (one lane per row), so that nothing serialises the groups.
                 float v[ILP];
@@ -458,11 +521,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const uint8_t *__re
     }
 }
 
-__global__ __launch_bounds__(256) void k_reduce(const float *__restrict__ partial, int n_chunks, int64_t R,
+__global__ __launch_bounds__(256) void k_reduce(const void *__restrict__ packed, ImageId id,
+                                                 const float *__restrict__ partial, int n_chunks, int64_t R,
                                                  float base, float *__restrict__ scores)
 {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= R) return;
+    if (!image_matches(packed, id)) {
+        scores[r] = __builtin_nanf("");
+        return;
+    }
     float acc = base;
     for (int c = 0; c < n_chunks; ++c) acc += partial[(int64_t)c * R + r];
     scores[r] = acc;
@@ -470,11 +538,17 @@ __global__ __launch_bounds__(256) void k_reduce(const float *__restrict__ partia
 
 // Four rows per thread with 16-byte loads (R % 4 == 0, so every chunk's
 // partial row starts 16-byte aligned); same chunk order per row.
-__global__ __launch_bounds__(256) void k_reduce4(const float *__restrict__ partial, int n_chunks, int64_t R,
+__global__ __launch_bounds__(256) void k_reduce4(const void *__restrict__ packed, ImageId id,
+                                                  const float *__restrict__ partial, int n_chunks, int64_t R,
                                                   float base, float *__restrict__ scores)
 {
     const int64_t r = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
     if (r >= R) return;
+    if (!image_matches(packed, id)) {
+        const float q = __builtin_nanf("");
+        *reinterpret_cast<float4 *>(scores + r) = make_float4(q, q, q, q);
+        return;
+    }
     float4 acc = make_float4(base, base, base, base);
 #pragma unroll 8
     for (int c = 0; c < n_chunks; ++c) {
@@ -488,34 +562,42 @@ __global__ __launch_bounds__(256) void k_reduce4(const float *__restrict__ parti
 }
 
 template <int TC, int D>
-hipError_t launch_traverse_tc(const uint8_t *chunks, int n_chunks, const uint8_t *Xb, int64_t R, int stride,
-                              float *partial, hipStream_t s)
+hipError_t launch_traverse_tc(const void *packed, ImageId id, const uint8_t *chunks, int n_chunks, const uint8_t *Xb,
+                              int64_t R, int stride, float *partial, const LeafHook &hook, hipStream_t s)
 {
     const int groups = n_chunks >= kSlotsPerXcd ? 1 : (kSlotsPerXcd + n_chunks - 1) / n_chunks;
     const int64_t n_groups = (int64_t)kXcds * groups;
     int64_t per = (R + n_groups - 1) / n_groups;
     per = (per + tile_rows(TC) - 1) / tile_rows(TC) * tile_rows(TC);
-    hipLaunchKernelGGL((k_traverse<TC, D>), dim3(kXcds * kSlotsPerXcd), dim3(64 * kWaves), 0, s, chunks,
-                       n_chunks, Xb, R, stride, groups, per, partial);
+    if (hook.hash || hook.idx)
+        hipLaunchKernelGGL((k_traverse<TC, D, true>), dim3(kXcds * kSlotsPerXcd), dim3(64 * kWaves), 0, s, packed,
+                           id, chunks, n_chunks, Xb, R, stride, groups, per, partial, hook);
+    else
+        hipLaunchKernelGGL((k_traverse<TC, D, false>), dim3(kXcds * kSlotsPerXcd), dim3(64 * kWaves), 0, s, packed,
+                           id, chunks, n_chunks, Xb, R, stride, groups, per, partial, hook);
     return hipGetLastError();
 }
 
-hipError_t launch_traverse(int depth, const uint8_t *chunks, int n_chunks, const uint8_t *Xb, int64_t R,
-                           int stride, float *partial, hipStream_t s)
+hipError_t launch_traverse(int depth, const void *packed, ImageId id, const uint8_t *chunks, int n_chunks,
+                           const uint8_t *Xb, int64_t R, int stride, float *partial, const LeafHook &hook,
+                           hipStream_t s)
 {
+#define HWSEL_TRAVERSE(TC_, D_) \
+    return launch_traverse_tc<TC_, D_>(packed, id, chunks, n_chunks, Xb, R, stride, partial, hook, s)
     switch (depth) {
-    case 1: return launch_traverse_tc<64, 1>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 2: return launch_traverse_tc<64, 2>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 3: return launch_traverse_tc<64, 3>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 4: return launch_traverse_tc<64, 4>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 5: return launch_traverse_tc<64, 5>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 6: return launch_traverse_tc<64, 6>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 7: return launch_traverse_tc<64, 7>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 8: return launch_traverse_tc<64, 8>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 9: return launch_traverse_tc<32, 9>(chunks, n_chunks, Xb, R, stride, partial, s);
-    case 10: return launch_traverse_tc<16, 10>(chunks, n_chunks, Xb, R, stride, partial, s);
+    case 1: HWSEL_TRAVERSE(64, 1);
+    case 2: HWSEL_TRAVERSE(64, 2);
+    case 3: HWSEL_TRAVERSE(64, 3);
+    case 4: HWSEL_TRAVERSE(64, 4);
+    case 5: HWSEL_TRAVERSE(64, 5);
+    case 6: HWSEL_TRAVERSE(64, 6);
+    case 7: HWSEL_TRAVERSE(64, 7);
+    case 8: HWSEL_TRAVERSE(64, 8);
+    case 9: HWSEL_TRAVERSE(32, 9);
+    case 10: HWSEL_TRAVERSE(16, 10);
     default: return hipErrorInvalidValue;
     }
+#undef HWSEL_TRAVERSE
 }
 
 }  // namespace
@@ -600,27 +682,52 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
             for (int64_t l = 0; l <= n_int; ++l) leaves[l * g.tc + tt] = leaf[tree * (n_int + 1) + l];
         }
     }
-    int32_t *hdr = reinterpret_cast<int32_t *>(img.data());
-    hdr[0] = 0x48575346;   // "FSWH"
-    hdr[1] = 2;
-    hdr[2] = f.n_trees; hdr[3] = f.depth; hdr[4] = f.n_features; hdr[5] = g.tc; hdr[6] = g.n_chunks;
+    const ImageId id = image_id(f, g);
+    std::memcpy(img.data(), &id, sizeof id);
     if (hipMemcpyAsync(packed, img.data(), g.total, hipMemcpyHostToDevice, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
         return PackStatus::hip_error;
     return PackStatus::ok;
 }
 
-const float *packed_thresholds(const void *packed)
-{
-    return reinterpret_cast<const float *>(static_cast<const uint8_t *>(packed) + 256);
-}
+ImageId packed_image_id(const hwsel_forest_t &f) { return image_id(f, geometry(f)); }
 
 int packed_bin_stride(const hwsel_forest_t &f) { return geometry(f).stride; }
 
 uint32_t packed_nan_bin(const hwsel_forest_t &f) { return (f.flags & 1u) ? 0u : 255u; }
 
+namespace {
+
+hipError_t traverse_and_reduce(const hwsel_forest_t &f, const void *packed, int64_t R, float *scores,
+                               void *workspace, const LeafHook &hook, hipStream_t s)
+{
+    const PackGeom g = geometry(f);
+    const ImageId id = image_id(f, g);
+    const uint8_t *chunks = static_cast<const uint8_t *>(packed) + 256 + g.thr_bytes;
+    const uint8_t *Xb = static_cast<const uint8_t *>(workspace);
+    float *partial = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + align256((size_t)R * g.stride));
+    hipError_t e = launch_traverse(f.depth, packed, id, chunks, g.n_chunks, Xb, R, g.stride, partial, hook, s);
+    if (e != hipSuccess) return e;
+    if (R % 4 == 0 && ((uintptr_t)scores & 15u) == 0)
+        hipLaunchKernelGGL(k_reduce4, dim3((unsigned)((R / 4 + 255) / 256)), dim3(256), 0, s, packed, id, partial,
+                           g.n_chunks, R, f.base_score, scores);
+    else
+        hipLaunchKernelGGL(k_reduce, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, packed, id, partial,
+                           g.n_chunks, R, f.base_score, scores);
+    return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
                                 int64_t ld, float *scores, void *workspace, hipStream_t s)
+{
+    return launch_forest_checked(f, packed, X, R, ld, scores, workspace, nullptr, nullptr, 0, 0, s);
+}
+
+hipError_t launch_forest_checked(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
+                                 int64_t ld, float *scores, void *workspace, uint64_t *leaf_hash,
+                                 uint16_t *leaf_idx, int64_t leaf_row0, int64_t leaf_rows, hipStream_t s)
 {
     const PackGeom g = geometry(f);
     uint8_t *Xb = static_cast<uint8_t *>(workspace);
@@ -628,30 +735,23 @@ hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, con
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
         n_cu = 256;
-    hipLaunchKernelGGL(k_bin, dim3(n_cu), dim3(kBinThreads), 0, s, X, R, ld, packed_thresholds(packed),
-                       f.n_features, packed_nan_bin(f), Xb, g.stride);
+    hipLaunchKernelGGL(k_bin, dim3(n_cu), dim3(kBinThreads), 0, s, X, R, ld, packed, image_id(f, g), f.n_features,
+                       packed_nan_bin(f), Xb, g.stride);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_forest_from_bins(f, packed, R, scores, workspace, s);
+    if (leaf_hash) {
+        hipLaunchKernelGGL(k_fill_u64, dim3(1024), dim3(256), 0, s, leaf_hash, R);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const LeafHook hook{leaf_hash, leaf_idx, leaf_row0, leaf_idx ? leaf_rows : 0, f.n_trees};
+    return traverse_and_reduce(f, packed, R, scores, workspace, hook, s);
 }
 
 // Traversal and reduction of bins already in the workspace.
 hipError_t launch_forest_from_bins(const hwsel_forest_t &f, const void *packed, int64_t R, float *scores,
                                    void *workspace, hipStream_t s)
 {
-    const PackGeom g = geometry(f);
-    const uint8_t *chunks = static_cast<const uint8_t *>(packed) + 256 + g.thr_bytes;
-    const uint8_t *Xb = static_cast<const uint8_t *>(workspace);
-    float *partial = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + align256((size_t)R * g.stride));
-    hipError_t e = launch_traverse(f.depth, chunks, g.n_chunks, Xb, R, g.stride, partial, s);
-    if (e != hipSuccess) return e;
-    if (R % 4 == 0 && ((uintptr_t)scores & 15u) == 0)
-        hipLaunchKernelGGL(k_reduce4, dim3((unsigned)((R / 4 + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
-                           f.base_score, scores);
-    else
-        hipLaunchKernelGGL(k_reduce, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, partial, g.n_chunks, R,
-                           f.base_score, scores);
-    return hipGetLastError();
+    return traverse_and_reduce(f, packed, R, scores, workspace, LeafHook{nullptr, nullptr, 0, 0, f.n_trees}, s);
 }
 
 }  // namespace hwsel

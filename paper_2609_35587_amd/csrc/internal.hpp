@@ -61,23 +61,42 @@ hipError_t launch_forest_leaves(const hwsel_forest_t &f, const float *X, int64_t
 
 // Packed forests (see forest.hip).
 enum class PackStatus { ok, hip_error, bad_feature, nan_threshold, too_many_thresholds };
+
+// Identity of a packed image, stored in its first 28 bytes (its threshold
+// table starts at byte 256); every kernel that reads an image compares it
+// with the forest the call is for first, and reads nothing more on a
+// mismatch.
+struct ImageId {
+    int32_t magic, version, n_trees, depth, n_features, tc, n_chunks;
+};
+
+__device__ __forceinline__ bool image_matches(const void *packed, const ImageId &want)
+{
+    const int32_t *h = static_cast<const int32_t *>(packed);
+    return h[0] == want.magic && h[1] == want.version && h[2] == want.n_trees && h[3] == want.depth &&
+           h[4] == want.n_features && h[5] == want.tc && h[6] == want.n_chunks;
+}
+
 bool packable(const hwsel_forest_t &f);
 size_t packed_bytes(const hwsel_forest_t &f);
 size_t packed_workspace_bytes(const hwsel_forest_t &f, int64_t R);
 PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s);
 hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
                                 int64_t ld, float *scores, void *workspace, hipStream_t s);
+hipError_t launch_forest_checked(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
+                                 int64_t ld, float *scores, void *workspace, uint64_t *leaf_hash,
+                                 uint16_t *leaf_idx, int64_t leaf_row0, int64_t leaf_rows, hipStream_t s);
 // Pieces of the packed path for the fused selection: the threshold table and
 // bin-row geometry of an image, and the traversal of bins already written to
 // the start of the workspace.
-const float *packed_thresholds(const void *packed);
+ImageId packed_image_id(const hwsel_forest_t &f);
 int packed_bin_stride(const hwsel_forest_t &f);
 uint32_t packed_nan_bin(const hwsel_forest_t &f);
 hipError_t launch_forest_from_bins(const hwsel_forest_t &f, const void *packed, int64_t R, float *scores,
                                    void *workspace, hipStream_t s);
 hipError_t launch_features_bins(const HwDev &hw, const hwsel_problem_t *problems, int32_t P, const int64_t *seg,
-                                const CandsDev &c, int64_t R, int32_t F, const float *U, int nf, uint32_t nan_bin,
-                                uint8_t *Xb, int stride, hipStream_t s);
+                                const CandsDev &c, int64_t R, int32_t F, const void *packed, ImageId id, int nf,
+                                uint32_t nan_bin, uint8_t *Xb, int stride, hipStream_t s);
 
 hipError_t launch_mlp(const hwsel_mlp_t &m, const float *X, int64_t R, int64_t ld, float *scores,
                       hipStream_t s);

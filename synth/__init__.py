@@ -361,14 +361,16 @@ def forest(cfg: Config, cuts: dict | None = None) -> dict:
                 node_feature=feat.astype(np.uint8), node_threshold=thr, leaf_value=leaves)
 
 
-def _bf16_bits_truncated(w: np.ndarray) -> np.ndarray:
-    """bf16 bit patterns of fp32 draws, keeping the top 16 bits."""
-    return (np.ascontiguousarray(w, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+def _bf16_bits_rounded(w: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of finite fp32 draws, rounded to nearest (ties to
+    even); a plain encoding of the generator's parameters."""
+    u = np.ascontiguousarray(w, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
 
 
 def mlp(cfg: Config, cuts: dict | None = None) -> dict:
     """Random MLP 128->512->512->256->1: Kaiming-normal weights (std
-    sqrt(2/fan_in)) stored as bf16 [out][in]; fp32 biases U(+-1/sqrt(fan_in));
+    sqrt(2/fan_in)) rounded to bf16, stored [out][in]; fp32 biases U(+-1/sqrt(fan_in));
     standardisation mean / 1/std taken from the stored column statistics
     (a column with zero spread gets 1/std = 0)."""
     if cuts is None:
@@ -378,7 +380,7 @@ def mlp(cfg: Config, cuts: dict | None = None) -> dict:
     for l in range(4):
         fi, fo = MLP_WIDTHS[l], MLP_WIDTHS[l + 1]
         w = rng.normal(0.0, np.sqrt(2.0 / fi), (fo, fi)).astype(np.float32)
-        out[f"W{l + 1}"] = _bf16_bits_truncated(w)
+        out[f"W{l + 1}"] = _bf16_bits_rounded(w)
         out[f"b{l + 1}"] = rng.uniform(-1.0 / np.sqrt(fi), 1.0 / np.sqrt(fi), fo).astype(np.float32)
     out["mean"] = cuts["mean"][:128].astype(np.float32)
     out["inv_std"] = cuts["inv_std"][:128].astype(np.float32)

@@ -241,3 +241,47 @@ def test_missing_library_fails_loudly():
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     out = subprocess.run(["python", "-c", code], capture_output=True, text=True, cwd=root, timeout=120)
     assert out.returncode == 0 and out.stdout.strip() == "raised", out.stderr
+
+
+def test_checked_scoring_rejects(L):
+    f = dict(n_trees=10, depth=6, n_features=64, flags=1, base_score=0.0, node_feature=FAKE,
+             node_threshold=FAKE, leaf_value=FAKE)
+    s = hwsel.forest_struct(f)
+    w = C.c_size_t(0)
+    assert L.hwsel_forest_workspace_bytes(C.byref(s), 100, C.byref(w)) == 0
+
+    def call(**over):
+        a = dict(packed=FAKE, X=FAKE, R=100, ld=64, scores=FAKE, ws=FAKE, wsb=w.value, lh=FAKE, li=None, r0=0, n=0)
+        a.update(over)
+        return L.hwsel_forest_score_checked(C.byref(s), a["packed"], a["X"], a["R"], a["ld"], a["scores"], a["ws"],
+                                            a["wsb"], a["lh"], a["li"], a["r0"], a["n"], None)
+
+    assert call(packed=None) == 1 and call(scores=None) == 1
+    assert call(wsb=w.value - 1) == 1 and call(ws=FAKE + 16) == 1
+    assert call(lh=FAKE + 4) == 1
+    assert call(li=FAKE, r0=-1, n=5) == 1 and call(li=FAKE, r0=96, n=5) == 1 and call(li=FAKE, r0=0, n=0) == 1
+    assert call(ld=63) == 1
+    assert L.hwsel_last_error().startswith(b"hwsel_forest_score_checked: ")
+
+
+def test_binding_rejects_host_tensors():
+    """A host tensor would hand a kernel a host pointer: the binding refuses
+    it (ValueError) before anything reaches the library."""
+    import numpy as np
+    import torch
+    X = torch.zeros((16, 64), dtype=torch.float32)
+    forest = dict(n_trees=2, depth=2, n_features=64, flags=1, base_score=0.0,
+                  node_feature=torch.zeros(6, dtype=torch.uint8), node_threshold=torch.zeros(6),
+                  leaf_value=torch.zeros(8))
+    for call in (lambda: hwsel.hwsel_forest_score(forest, X),
+                 lambda: hwsel.hwsel_topk_per_problem(torch.zeros(16), torch.tensor([0, 16]), 3),
+                 lambda: hwsel.hwsel_regret(torch.zeros(16), torch.tensor([0, 16]),
+                                            torch.zeros((1, 3), dtype=torch.int32)),
+                 lambda: hwsel.hwsel_evaluate(torch.zeros(16), torch.tensor([0, 16]),
+                                              torch.zeros((1, 3), dtype=torch.int32)),
+                 lambda: hwsel.hwsel_linear_score(dict(n_features=64, bias=0.0, mean=torch.zeros(64),
+                                                       inv_std=torch.zeros(64), w=torch.zeros(64),
+                                                       w_onehot=torch.zeros(12)), X)):
+        with pytest.raises(ValueError):
+            call()
+    del np

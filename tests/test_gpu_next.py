@@ -314,3 +314,36 @@ def test_catalogue_rows_any_field_alignment():
             for n in hwsel.CAND_FIELDS:
                 got = c[n].cpu().numpy()[seg[p]:seg[p + 1]]
                 assert np.array_equal(got.view(ref[n].dtype), ref[n]), (off, p, n)
+
+
+# ----------------------------------------------------------------------------
+# binding: short, mistyped or misplaced buffers are refused before any launch
+# ----------------------------------------------------------------------------
+def test_binding_rejects_bad_buffers():
+    w = synth.workload("tiny")
+    d = Dev(w)
+    R = w.cfg.rows
+    X = d.features(64)
+    dev = X.device
+    bad = [
+        lambda: hwsel.hwsel_features(w.hw, d.problems, d.seg, d.cands, 64, X=torch.empty((R - 1, 64), device=dev)),
+        lambda: hwsel.hwsel_features(w.hw, d.problems, d.seg, d.cands, 64, X=torch.empty((R, 64), device=dev,
+                                                                                         dtype=torch.float64)),
+        lambda: hwsel.hwsel_forest_score(d.forest, X, scores=torch.empty(R - 1, device=dev)),
+        lambda: hwsel.hwsel_forest_score(d.forest, X[:, :32]),
+        lambda: hwsel.hwsel_forest_score(d.forest, X, packed=torch.empty(100, dtype=torch.uint8, device=dev)),
+        lambda: hwsel.hwsel_topk_per_problem(torch.zeros(R, device=dev), d.seg, 5,
+                                             idx=torch.empty((w.cfg.n_problems, 4), dtype=torch.int32, device=dev)),
+        lambda: hwsel.hwsel_topk_per_problem(torch.zeros(R, device=dev), d.seg, 5,
+                                             idx=torch.empty((w.cfg.n_problems, 5), dtype=torch.int64, device=dev)),
+        lambda: hwsel.hwsel_regret(d.runtimes, d.seg, torch.zeros((w.cfg.n_problems, 5), dtype=torch.int32,
+                                                                  device=dev), r1=torch.empty(3, device=dev)),
+        lambda: hwsel.hwsel_mlp_score(mlp_dev, torch.zeros((10, 128), device=dev), scores=torch.empty(9, device=dev)),
+        lambda: hwsel.hwsel_catalogue_compact(torch.zeros((2, 10), dtype=torch.uint8, device=dev),
+                                              torch.zeros(2, dtype=torch.int64, device=dev), 5),
+    ]
+    mlp_dev = {k: up(v) for k, v in synth.mlp(synth.CONFIGS["mlp"]).items()}
+    for i, call in enumerate(bad):
+        with pytest.raises(ValueError):
+            call()
+            say(f"  case {i} was not refused")

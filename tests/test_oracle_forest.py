@@ -85,3 +85,30 @@ def test_row_subset_matches_full():
     X = rng.standard_normal((50, 4)).astype(np.float32)
     rows = np.array([49, 3, 17, 17], np.int64)
     assert np.array_equal(oracle.forest(f, X, rows=rows), oracle.forest(f, X)[rows])
+
+
+def test_leaf_mix_is_splitmix64_finaliser():
+    # SplitMix64 seeded with 0 returns mix(g), mix(2g), ... with the golden
+    # gamma g = 0x9E3779B97F4A7C15; its first two published outputs
+    g = 0x9E3779B97F4A7C15
+    assert oracle.leaf_mix(g) == 0xE220A8397B1DCDAF
+    assert oracle.leaf_mix(2 * g) == 0x6E789E6AA1B965F4
+    assert oracle.leaf_mix(0) == 0
+
+
+def test_leaf_hash_is_sum_of_mixed_tree_leaf_pairs():
+    rng = np.random.default_rng(21)
+    depth, T, F = 4, 9, 5
+    n_int = (1 << depth) - 1
+    f = forest(rng.integers(0, F, (T, n_int)), rng.standard_normal(T * n_int), rng.standard_normal(T << depth),
+               depth, n_features=F)
+    X = rng.standard_normal((40, F)).astype(np.float32)
+    s, li, h = oracle.forest(f, X, leaves=True, leaf_hash=True)
+    assert np.array_equal(s, oracle.forest(f, X))
+    for r in range(40):
+        want = sum(oracle.leaf_mix((t << 32) | int(li[r, t])) for t in range(T)) % (1 << 64)
+        assert int(h[r]) == want
+    # one changed leaf changes the fingerprint; the tree order does not matter
+    # for it, only which leaf each tree reaches
+    alt = (int(h[0]) - oracle.leaf_mix(int(li[0, 3])) + oracle.leaf_mix((3 << 32) | (int(li[0, 3]) ^ 1))) % (1 << 64)
+    assert alt != int(h[0])
