@@ -35,11 +35,16 @@ sys.path.insert(0, ROOT)
 
 METRIC = "candidate rows scored/sec (features+forest+top-k) at 4.9M rows; % HBM roofline"
 HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
 # VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
 LANE_OPS_PER_S = 256 * 64 * 2.4e9
-# an exact traversal step issues at least 4 VALU lane-ops per node visit
-# (child index, node address, feature address, compare)
-MIN_OPS_PER_VISIT = 4
+# the traversal's walk issues 5 VALU instructions per node visit (compare with
+# borrow, child-code select, child index with carry, bin address, pair
+# address: counted in its ISA) and 1.8 LDS gathers (bin, and the sibling pair
+# on 7 of 10 levels); LDS serves 32 lanes per clock per CU
+VALU_OPS_PER_VISIT = 5
+LDS_LANES_PER_S = 256 * 32 * 2.4e9
+LDS_OPS_PER_VISIT = 1.8
 
 
 def forest_traffic_bytes():
@@ -62,6 +67,87 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def ceilings(torch) -> dict:
+    """Measured ceilings (libhwsel_ceilings.so): the traversal's own walk with
+    every operand in LDS, back-to-back bf16 matrix-core products, and a
+    streaming copy, each timed with HIP events on the current stream."""
+    import ctypes as C
+    path = os.path.join(ROOT, "paper_2609_35587_amd", "libhwsel_ceilings.so")
+    L = C.CDLL(path)
+    L.hwsel_ceiling_visits_per_launch.restype = C.c_int64
+    L.hwsel_ceiling_mfma_flops_per_launch.restype = C.c_double
+    L.hwsel_ceiling_visits.argtypes = [C.c_int, C.c_void_p, C.c_void_p]
+    L.hwsel_ceiling_mfma.argtypes = [C.c_int, C.c_void_p, C.c_void_p]
+    L.hwsel_ceiling_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]
+    stream = torch.cuda.current_stream()
+    sink = torch.zeros(16, dtype=torch.float32, device="cuda")
+    h = stream.cuda_stream
+
+    def best(fn, reps=5):
+        fn()
+        out = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1) / 1e3)
+        return min(out)
+
+    it_v, it_m = 2000, 20000
+    t_v = best(lambda: L.hwsel_ceiling_visits(it_v, sink.data_ptr(), h))
+    t_m = best(lambda: L.hwsel_ceiling_mfma(it_m, sink.data_ptr(), h))
+    n16 = (1 << 30) // 16
+    src = torch.ones(n16 * 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    t_c = best(lambda: L.hwsel_ceiling_copy(src.data_ptr(), dst.data_ptr(), n16, h))
+    del src, dst
+    return {"visits_per_s": L.hwsel_ceiling_visits_per_launch(it_v) / t_v,
+            "bf16_flops_per_s": L.hwsel_ceiling_mfma_flops_per_launch(it_m) / t_m,
+            "copy_GBps": 2 * (1 << 30) / t_c / 1e9}
+
+
+def per_config(hwsel, torch, dev, name: str) -> dict:
+    """The scored path (features, packed forest, top-k, regret) on one of the
+    other workloads, each stage timed on its own (median of 3)."""
+    import synth
+    w = synth.workload(name)
+    cfg = w.cfg
+    R, P, F, k = cfg.rows, cfg.n_problems, cfg.n_features, cfg.k
+    probs, seg = hwsel.to_device(w.problems, dev), hwsel.to_device(w.seg, dev)
+    cands = {n: hwsel.to_device(v, dev) for n, v in w.cands.items()}
+    rt = hwsel.to_device(w.runtimes, dev)
+    forest = dict(w.forest)
+    for n in ("node_feature", "node_threshold", "leaf_value"):
+        forest[n] = hwsel.to_device(w.forest[n], dev)
+    packed = hwsel.hwsel_forest_pack(forest)
+    ws = torch.empty(hwsel.hwsel_forest_workspace_bytes(forest, R), dtype=torch.uint8, device=dev)
+    X = torch.empty((R, F), dtype=torch.float32, device=dev)
+    s = torch.empty(R, dtype=torch.float32, device=dev)
+    idx = torch.empty((P, k), dtype=torch.int32, device=dev)
+    out = {"rows": R, "problems": P, "features": F, "trees": cfg.trees, "depth": cfg.depth, "k": k}
+    out["features_ms"] = timed(torch, lambda: hwsel.hwsel_features(w.hw, probs, seg, cands, F, X=X))
+    out["forest_ms"] = timed(torch, lambda: hwsel.hwsel_forest_score(forest, X, scores=s, packed=packed, workspace=ws))
+    out["topk_ms"] = timed(torch, lambda: hwsel.hwsel_topk_per_problem(s, seg, k, idx=idx, with_vals=False))
+    out["regret_ms"] = timed(torch, lambda: hwsel.hwsel_regret(rt, seg, idx))
+    path_ms = out["features_ms"] + out["forest_ms"] + out["topk_ms"]
+    out["rows_per_s"] = R / (path_ms / 1e3)
+    out["visits_per_s"] = R * cfg.trees * cfg.depth / (out["forest_ms"] / 1e3)
+    out["features_hbm_frac"] = R * (17 + 4 * F) / (out["features_ms"] / 1e3) / 1e9 / HBM_PEAK_GBS
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, n_problems: int) -> dict:
     import oracle
     cfg = w.cfg
@@ -81,6 +167,7 @@ def cpu_baseline(w, n_problems: int) -> dict:
     oracle.regret(w.runtimes[:R], seg, idx2)
     dt = time.perf_counter() - t0
     return {"value": R / dt, "unit": "rows/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"first {n_problems} of {cfg.n_problems} problems ({R} rows), whole path "
                       f"(features, forest, MLP, top-{cfg.k}, regret), {dt:.1f} s"}
 
@@ -257,7 +344,10 @@ def main():
     visits = R * cfg.trees * cfg.depth
     t_forest = per_stage["forest"] / 1e3
     visit_rate = visits / t_forest
-    peak_visits = LANE_OPS_PER_S / MIN_OPS_PER_VISIT
+    peak_visits = min(LANE_OPS_PER_S / VALU_OPS_PER_VISIT, LDS_LANES_PER_S / LDS_OPS_PER_VISIT)
+    log("measured ceilings")
+    ceil = ceilings(torch)
+    mlp_flops = R * 918016 / (per_stage["mlp"] / 1e3)
     # algorithmic HBM bytes of the whole step: candidate records (17 B) + X write
     # (4F) + X read by forest and MLP (2 x 4F) + two score vectors written and
     # read (4 x 4 B) + runtimes read twice (2 x 4 B)
@@ -278,11 +368,33 @@ def main():
                      "achieved": visit_rate / 1e9, "peak": peak_visits / 1e9, "unit": "Gvisits/s",
                      "frac": visit_rate / peak_visits, "traffic": forest_traffic_bytes(),
                      "visits_per_launch": visits,
+                     "measured_ceiling": ceil["visits_per_s"] / 1e9,
+                     "frac_of_measured_ceiling": visit_rate / ceil["visits_per_s"],
                      "hbm_frac": forest_bytes / t_forest / 1e9 / HBM_PEAK_GBS},
+        "rooflines_other": {
+            "mlp": {"kernel": "hwsel_mlp_score (k_mlp_mfma)", "bound": "mfma", "unit": "TFLOP/s",
+                    "achieved": mlp_flops / 1e12, "peak": BF16_PEAK_TFLOPS,
+                    "frac": mlp_flops / 1e12 / BF16_PEAK_TFLOPS,
+                    "measured_ceiling": ceil["bf16_flops_per_s"] / 1e12,
+                    "frac_of_measured_ceiling": mlp_flops / ceil["bf16_flops_per_s"]},
+            "features": {"kernel": "hwsel_features (k_features<128>)", "bound": "hbm", "unit": "GB/s",
+                         "achieved": R * (17 + 4 * F) / (per_stage["features"] / 1e3) / 1e9, "peak": HBM_PEAK_GBS,
+                         "frac": R * (17 + 4 * F) / (per_stage["features"] / 1e3) / 1e9 / HBM_PEAK_GBS,
+                         "measured_ceiling": ceil["copy_GBps"],
+                         "frac_of_measured_ceiling": R * (17 + 4 * F) / (per_stage["features"] / 1e3) / 1e9
+                         / ceil["copy_GBps"]},
+        },
+        "measured_ceilings": {"visits_per_s": ceil["visits_per_s"], "bf16_flops_per_s": ceil["bf16_flops_per_s"],
+                              "copy_GBps": ceil["copy_GBps"]},
     }
     if not a.no_extras:
         line["extras"] = extras(a, w, hwsel, torch, dev, probs, seg, cands, rt, forest, packed, X, outs[0][0],
                                 per_stage)
+        del X, ws, s_f, s_m
+        for name in ("tiny", "medium", "full"):
+            log(f"extras: {name} workload")
+            line["extras"][f"workload_{name}"] = per_config(hwsel, torch, dev, name)
+            torch.cuda.empty_cache()
     if not a.no_cpu_baseline:
         log(f"cpu baseline: oracle on {a.cpu_problems} problems")
         line["cpu_baseline"] = cpu_baseline(w, a.cpu_problems)
