@@ -3,12 +3,14 @@
 // One workgroup per problem segment.  Scores are mapped to 64-bit keys
 // (order-preserving score bits << 32 | inverted local index), which makes
 // every key unique: "score descending, index ascending" becomes "key
-// descending" and the answer is unique.  The k best keys are found by k
+// descending" and the answer is unique.  The k best keys are found by
 // rounds of a block-wide maximum restricted to keys below the previous
 // winner.  A segment of up to 8,192 rows is read once into registers (32
-// keys per thread); a longer one is read k times, from L2 after the first
-// round.  The wave maximum of a 64-bit key runs on DPP: the high words'
-// maximum, then the low words of the lanes that hold it.
+// keys per thread) and gives its k best in k rounds; a longer one is read
+// once too, tile by tile, keeping a running list of the k best: a tile's
+// rounds extract only its keys above the list's k-th entry and stop at the
+// first round that finds none.  The wave maximum of a 64-bit key runs on
+// DPP: the high words' maximum, then the low words of the lanes that hold it.
 #include "internal.hpp"
 
 namespace hwsel {
@@ -127,16 +129,56 @@ __global__ __launch_bounds__(kThreads) void k_topk(const float *__restrict__ sco
             prev = best;
         }
     } else {
-        for (int32_t j = 0; j < k; ++j) {
-            uint64_t best = 0;
-            for (int64_t i = threadIdx.x; i < n; i += kThreads) {
-                const uint64_t key = key_of(i);
-                best = (key < prev && key > best) ? key : best;
+        // Longer segments are read once, in tiles of kThreads * kRegRows keys
+        // held in registers.  top[0..kept) is the running list of the k best
+        // keys (descending); from each tile only the keys above its k-th entry
+        // (floor, 0 until k rows are kept) are extracted, largest first, and
+        // the rounds stop as soon as none is left, then wave 0 merges them in
+        // by rank (keys are unique, so ranks are exact).
+        __shared__ uint64_t top[64], cand[64];
+        __shared__ int32_t kept_s;
+        if (threadIdx.x == 0) kept_s = 0;
+        uint64_t floor = 0;
+        int32_t kept = 0;
+        for (int64_t t0 = 0; t0 < n; t0 += (int64_t)kThreads * kRegRows) {
+            uint64_t key[kRegRows];
+#pragma unroll
+            for (int r = 0; r < kRegRows; ++r) {
+                const int64_t i = t0 + threadIdx.x + (int64_t)r * kThreads;
+                key[r] = i < n ? key_of(i) : 0ull;
             }
-            best = block_max_key(best, sh[j & 1]);
-            emit(j, best);
-            prev = best;
+            int32_t m = 0;
+            uint64_t c_prev = ~0ull;
+            for (; m < k; ++m) {                          // block-uniform trip count
+                uint64_t best = 0;
+#pragma unroll
+                for (int r = 0; r < kRegRows; ++r)
+                    best = (key[r] < c_prev && key[r] > floor && key[r] > best) ? key[r] : best;
+                best = block_max_key(best, sh[m & 1]);
+                if (best == 0) break;
+                if (threadIdx.x == 0) cand[m] = best;
+                c_prev = best;
+            }
+            __syncthreads();
+            if (threadIdx.x < 64 && m > 0) {
+                // merged rank of each entry = its own index + the number of
+                // entries of the other list above it
+                const int lane = threadIdx.x;
+                uint64_t mine_t = lane < kept ? top[lane] : 0ull, mine_c = lane < m ? cand[lane] : 0ull;
+                int32_t rank_t = lane, rank_c = lane;
+                for (int32_t q = 0; q < m; ++q) rank_t += cand[q] > mine_t;
+                for (int32_t q = 0; q < kept; ++q) rank_c += top[q] > mine_c;
+                __builtin_amdgcn_wave_barrier();
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // every lane has read both lists
+                if (lane < kept && rank_t < k) top[rank_t] = mine_t;
+                if (lane < m && rank_c < k) top[rank_c] = mine_c;
+                if (lane == 0) kept_s = kept + m < k ? kept + m : k;
+            }
+            __syncthreads();
+            kept = kept_s;
+            if (kept == k) floor = top[k - 1];
         }
+        for (int32_t j = 0; j < k; ++j) emit(j, j < kept ? top[j] : 0ull);
     }
 }
 

@@ -155,6 +155,32 @@ def test_topk_single_long_segment_and_all_ties():
     assert oidx[0, 0] == 12345 and oidx[0, 1:].tolist() == list(range(63))
 
 
+@pytest.mark.parametrize("k", [1, 16, 64])
+def test_topk_long_segments_tile_merge(k):
+    """Segments longer than one register tile (8,192 rows): read once, tile
+    by tile, with a running list of the k best -- against the oracle's full
+    sort on orders that stress the merge (best rows last, first, spread over
+    tiles; heavy ties; NaN and infinities) and lengths around tile edges."""
+    say(f"topk long segments k={k}")
+    rng = np.random.default_rng(500 + k)
+    lens = [8193, 16384, 16385, 40000, 65536, 8192 * 5 + 3, 100, 0, 70001]
+    seg = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    R = int(seg[-1])
+    s = synth.random_scores(rng, R, tie_frac=0.3, n_levels=5)
+    a0, a1, a2, a3 = seg[0], seg[1], seg[2], seg[3]
+    s[a0:a1] = np.arange(a1 - a0, dtype=np.float32)             # ascending: every tile beats the last
+    s[a1:a2] = -np.arange(a2 - a1, dtype=np.float32)            # descending: the first tile wins
+    s[a2:a3] = 7.0                                              # all ties: lowest indices win
+    b = seg[4]
+    s[b:b + 50] = np.nan
+    s[b + 60000] = np.inf
+    s[b + 30000] = -np.inf
+    idx, vals = hwsel.hwsel_topk_per_problem(torch.from_numpy(s).cuda(), torch.from_numpy(seg).cuda(), k)
+    oidx, ovals = oracle.topk(s, seg, k)
+    assert np.array_equal(idx.cpu().numpy(), oidx)
+    assert np.array_equal(vals.cpu().numpy().view(np.uint32), ovals.view(np.uint32))
+
+
 # ----------------------------------------------------------------------------
 # Full-size workloads: sampled rows + properties
 # ----------------------------------------------------------------------------
