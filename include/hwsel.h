@@ -150,6 +150,12 @@ typedef struct hwsel_forest {
  */
 int hwsel_forest_pack_bytes(const hwsel_forest_t *f, size_t *bytes);
 int hwsel_forest_pack(const hwsel_forest_t *f, void *packed, size_t bytes, void *stream);
+/* The same image built from a forest whose arrays (node_feature,
+ * node_threshold, leaf_value) are in HOST memory, written to `image` (host
+ * memory of hwsel_forest_pack_bytes() bytes); no HIP call is made, so it
+ * runs on a machine without a GPU.  Copy the image to device memory (16-byte
+ * aligned) to score with it.  Same status codes as hwsel_forest_pack. */
+int hwsel_forest_pack_host(const hwsel_forest_t *f, void *image, size_t bytes);
 
 /* Device workspace (bytes) hwsel_forest_score needs for a packed forest and
  * R rows: u8 bins [R][n_features rounded up to 16] and one fp32 partial sum

@@ -279,6 +279,25 @@ int hwsel_forest_pack(const hwsel_forest_t *f, void *packed, size_t bytes, void 
     }
 }
 
+int hwsel_forest_pack_host(const hwsel_forest_t *f, void *image, size_t bytes)
+{
+    static const char *fn = "hwsel_forest_pack_host";
+    size_t need = 0;
+    if (int s = hwsel_forest_pack_bytes(f, &need)) return s;
+    if (!image || !f->node_feature || !f->node_threshold || !f->leaf_value)
+        return fail(HWSEL_EINVAL, fn, "null pointer");
+    if (f->n_features < 1 || f->depth < 1) return fail(HWSEL_EINVAL, fn, "empty forest shape");
+    if (bytes < need) return fail(HWSEL_EINVAL, fn, "bytes=%zu < %zu", bytes, need);
+    switch (hwsel::build_image(*f, f->node_feature, f->node_threshold, f->leaf_value, static_cast<uint8_t *>(image))) {
+    case hwsel::PackStatus::ok: g_err[0] = 0; return HWSEL_OK;
+    case hwsel::PackStatus::bad_feature: return fail(HWSEL_EINVAL, fn, "node feature >= n_features");
+    case hwsel::PackStatus::nan_threshold: return fail(HWSEL_EINVAL, fn, "NaN threshold");
+    case hwsel::PackStatus::too_many_thresholds:
+        return fail(HWSEL_EUNSUPPORTED, fn, "a feature has more than 255 distinct thresholds");
+    default: return fail(HWSEL_EINVAL, fn, "cannot pack");
+    }
+}
+
 int hwsel_forest_workspace_bytes(const hwsel_forest_t *f, int64_t R, size_t *bytes)
 {
     static const char *fn = "hwsel_forest_workspace_bytes";

@@ -632,19 +632,15 @@ size_t packed_workspace_bytes(const hwsel_forest_t &f, int64_t R)
     return align256((size_t)R * g.stride) + (size_t)g.n_chunks * (size_t)R * sizeof(float);
 }
 
-// Copy the forest to the host, build the binned chunk images, upload them.
-PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
+// The packed image of a forest whose arrays are in host memory, written to
+// img (host memory of packed_bytes(f) bytes): per-feature sorted distinct
+// thresholds, then the chunks of sibling-pair codes and leaves.
+PackStatus build_image(const hwsel_forest_t &f, const uint8_t *feat, const float *thr, const float *leaf,
+                       uint8_t *img_out)
 {
     const PackGeom g = geometry(f);
     const int64_t n_int = ((int64_t)1 << f.depth) - 1;
-    const int64_t nn = n_int * f.n_trees, nl = (n_int + 1) * f.n_trees;
-    std::vector<uint8_t> feat(nn);
-    std::vector<float> thr(nn), leaf(nl);
-    if (hipMemcpyAsync(feat.data(), f.node_feature, nn, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipMemcpyAsync(thr.data(), f.node_threshold, nn * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipMemcpyAsync(leaf.data(), f.leaf_value, nl * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
-        return PackStatus::hip_error;
+    const int64_t nn = n_int * f.n_trees;
     // distinct thresholds per feature
     std::vector<std::vector<float>> U(f.n_features);
     for (int64_t e = 0; e < nn; ++e) {
@@ -684,6 +680,25 @@ PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
     }
     const ImageId id = image_id(f, g);
     std::memcpy(img.data(), &id, sizeof id);
+    std::memcpy(img_out, img.data(), g.total);
+    return PackStatus::ok;
+}
+
+// Copy the forest to the host, build the image there, upload it.
+PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s)
+{
+    const PackGeom g = geometry(f);
+    const int64_t n_int = ((int64_t)1 << f.depth) - 1;
+    const int64_t nn = n_int * f.n_trees, nl = (n_int + 1) * f.n_trees;
+    std::vector<uint8_t> feat(nn), img(g.total);
+    std::vector<float> thr(nn), leaf(nl);
+    if (hipMemcpyAsync(feat.data(), f.node_feature, nn, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(thr.data(), f.node_threshold, nn * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(leaf.data(), f.leaf_value, nl * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return PackStatus::hip_error;
+    const PackStatus st = build_image(f, feat.data(), thr.data(), leaf.data(), img.data());
+    if (st != PackStatus::ok) return st;
     if (hipMemcpyAsync(packed, img.data(), g.total, hipMemcpyHostToDevice, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
         return PackStatus::hip_error;

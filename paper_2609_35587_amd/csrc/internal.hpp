@@ -81,6 +81,8 @@ bool packable(const hwsel_forest_t &f);
 size_t packed_bytes(const hwsel_forest_t &f);
 size_t packed_workspace_bytes(const hwsel_forest_t &f, int64_t R);
 PackStatus pack_forest(const hwsel_forest_t &f, void *packed, hipStream_t s);
+PackStatus build_image(const hwsel_forest_t &f, const uint8_t *feat, const float *thr, const float *leaf,
+                       uint8_t *img);
 hipError_t launch_forest_packed(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,
                                 int64_t ld, float *scores, void *workspace, hipStream_t s);
 hipError_t launch_forest_checked(const hwsel_forest_t &f, const void *packed, const float *X, int64_t R,

@@ -82,6 +82,7 @@ def lib() -> C.CDLL:
         L.hwsel_forest_score.argtypes = [C.POINTER(hwsel_forest_t), vp, vp, i64, i64, vp, vp, C.c_size_t, vp]
         L.hwsel_forest_pack_bytes.argtypes = [C.POINTER(hwsel_forest_t), C.POINTER(C.c_size_t)]
         L.hwsel_forest_pack.argtypes = [C.POINTER(hwsel_forest_t), vp, C.c_size_t, vp]
+        L.hwsel_forest_pack_host.argtypes = [C.POINTER(hwsel_forest_t), vp, C.c_size_t]
         L.hwsel_forest_workspace_bytes.argtypes = [C.POINTER(hwsel_forest_t), i64, C.POINTER(C.c_size_t)]
         L.hwsel_forest_score_checked.argtypes = [C.POINTER(hwsel_forest_t), vp, vp, i64, i64, vp, vp, C.c_size_t,
                                                  vp, vp, i64, i64, vp]
@@ -291,6 +292,20 @@ def _forest_arrays(forest: dict) -> None:
 
 def _packed_image(forest: dict, packed: torch.Tensor, like: torch.Tensor) -> None:
     _arg(packed, "packed", U8, hwsel_forest_pack_bytes(forest), like)
+
+
+def hwsel_forest_pack_host(forest: dict) -> np.ndarray:
+    """The packed image of a forest given as host numpy arrays, built on the
+    host (no GPU needed); returns it as uint8 numpy array."""
+    arrays = {n: np.ascontiguousarray(forest[n], dt) for n, dt in
+              (("node_feature", np.uint8), ("node_threshold", np.float32), ("leaf_value", np.float32))}
+    f = dict(forest, **{n: a.ctypes.data for n, a in arrays.items()})
+    n = C.c_size_t(0)
+    s = forest_struct(f)
+    _check("hwsel_forest_pack_bytes", lib().hwsel_forest_pack_bytes(C.byref(s), C.byref(n)))
+    image = np.zeros(int(n.value), np.uint8)
+    _check("hwsel_forest_pack_host", lib().hwsel_forest_pack_host(C.byref(s), image.ctypes.data, image.size))
+    return image
 
 
 def hwsel_forest_workspace_bytes(forest: dict, R: int) -> int:

@@ -391,3 +391,14 @@ def test_forest_every_depth(depth, trees, flags):
     li = hwsel.hwsel_forest_leaves(fd, Xd, rows).cpu().numpy().view(np.uint16)
     assert np.array_equal(li, oli[::7])
     say(f"  err/bound direct {e_direct:.3g} packed {e_packed:.3g}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "dataset"])
+def test_forest_pack_host_equals_device_pack(name):
+    """hwsel_forest_pack (device arrays) and hwsel_forest_pack_host (host
+    arrays, no GPU) write the same image, byte for byte."""
+    from _gpu_util import forest_to_device
+    f = synth.forest(synth.CONFIGS[name])
+    dev_img = hwsel.hwsel_forest_pack(forest_to_device(f)).cpu().numpy()
+    host_img = hwsel.hwsel_forest_pack_host(f)
+    assert np.array_equal(dev_img, host_img)
