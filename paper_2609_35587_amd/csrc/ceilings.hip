@@ -12,8 +12,10 @@
 //                    rows are refilled and no partial sums stored.
 //   k_mfma_ceiling   back-to-back independent v_mfma_f32_32x32x16_bf16 on
 //                    register operands (four accumulators per wave).
-//   k_copy_ceiling   a streaming 16-byte-per-lane device copy (HBM read and
-//                    write rate).
+//   k_copy_ceiling   a streaming device copy, 16 bytes per lane, four in
+//                    flight (HBM read + write rate);
+//   k_fill_ceiling   a streaming device fill (HBM write rate; the runtime's
+//                    own fill is timed beside it and the faster one kept).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -173,10 +175,29 @@ __global__ __launch_bounds__(256) void k_mfma_ceiling(int iters, float *sink)
     if (s == 1234.5f) sink[0] = s;
 }
 
-__global__ __launch_bounds__(256) void k_copy_ceiling(const uint4 *__restrict__ src, uint4 *__restrict__ dst, int64_t n)
+// Streaming copy and fill: each thread moves 4 x 16 bytes per step, all
+// loads of a step issued before its stores (the tail is guarded).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void k_copy_ceiling(const u32x4 *__restrict__ src, u32x4 *__restrict__ dst, int64_t n)
 {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += 4 * stride) {
+        u32x4 v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (i + q * stride < n) v[q] = __builtin_nontemporal_load(src + i + q * stride);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (i + q * stride < n) __builtin_nontemporal_store(v[q], dst + i + q * stride);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_fill_ceiling(u32x4 *__restrict__ dst, int64_t n)
+{
+    const u32x4 z = {0u, 0u, 0u, 0u};
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
+        __builtin_nontemporal_store(z, dst + i);
 }
 
 int n_cus()
@@ -213,8 +234,20 @@ int hwsel_ceiling_mfma(int iters, float *sink, void *stream)
 // Copies n16 16-byte elements (both buffers device memory, 16-byte aligned).
 int hwsel_ceiling_copy(const void *src, void *dst, int64_t n16, void *stream)
 {
-    hipLaunchKernelGGL(k_copy_ceiling, dim3(8 * n_cus()), dim3(256), 0, (hipStream_t)stream,
-                       static_cast<const uint4 *>(src), static_cast<uint4 *>(dst), n16);
+    hipLaunchKernelGGL(k_copy_ceiling, dim3(64 * n_cus()), dim3(256), 0, (hipStream_t)stream,
+                       static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), n16);
+    return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+// Writes n16 16-byte zeros (device memory, 16-byte aligned): with the
+// kernel above (runtime = 0) or with the HIP runtime's own fill (runtime = 1,
+// hipMemsetD32Async), whichever the caller times.
+int hwsel_ceiling_fill(void *dst, int64_t n16, int runtime, void *stream)
+{
+    if (runtime)
+        return hipMemsetD32Async((hipDeviceptr_t)dst, 0, (size_t)n16 * 4, (hipStream_t)stream) == hipSuccess ? 0 : 3;
+    hipLaunchKernelGGL(k_fill_ceiling, dim3(64 * n_cus()), dim3(256), 0, (hipStream_t)stream,
+                       static_cast<u32x4 *>(dst), n16);
     return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 
