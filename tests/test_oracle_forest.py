@@ -110,5 +110,9 @@ def test_leaf_hash_is_sum_of_mixed_tree_leaf_pairs():
         assert int(h[r]) == want
     # one changed leaf changes the fingerprint; the tree order does not matter
     # for it, only which leaf each tree reaches
-    alt = (int(h[0]) - oracle.leaf_mix(int(li[0, 3])) + oracle.leaf_mix((3 << 32) | (int(li[0, 3]) ^ 1))) % (1 << 64)
+    alt = (int(h[0]) - oracle.leaf_mix((3 << 32) | int(li[0, 3]))
+           + oracle.leaf_mix((3 << 32) | (int(li[0, 3]) ^ 1))) % (1 << 64)
     assert alt != int(h[0])
+    # the same leaf reached in another tree is another term: the fingerprint
+    # tells which tree reached which leaf
+    assert oracle.leaf_mix((3 << 32) | 5) != oracle.leaf_mix((4 << 32) | 5)
