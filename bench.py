@@ -152,7 +152,11 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, n_problems: int) -> dict:
+def cpu_baseline(w, n_problems: int, gpu_idx_forest: np.ndarray, gpu_idx_mlp: np.ndarray) -> tuple[dict, dict]:
+    """Times the oracle on the first n_problems problems of the workload and
+    compares its picks there with the library's from the timed step (problems
+    whose forest top-k, MLP top-1 and MLP top-k equal the oracle's).  Returns
+    the baseline record and the comparison."""
     import oracle
     cfg = w.cfg
     seg = w.seg[: n_problems + 1]
@@ -170,10 +174,15 @@ def cpu_baseline(w, n_problems: int) -> dict:
     idx2, _ = oracle.topk(sm, seg, cfg.k)
     oracle.regret(w.runtimes[:R], seg, idx2)
     dt = time.perf_counter() - t0
+    gf, gm = gpu_idx_forest[:n_problems], gpu_idx_mlp[:n_problems]
+    parity = {"problems": n_problems,
+              "forest_topk_equal": int(sum(np.array_equal(gf[p], idx[p]) for p in range(n_problems))),
+              "mlp_top1_equal": int(np.sum(gm[:, 0] == idx2[:, 0])),
+              "mlp_topk_equal": int(sum(np.array_equal(gm[p], idx2[p]) for p in range(n_problems)))}
     return {"value": R / dt, "unit": "rows/s", "cores": oracle.num_threads(), "kind": "oracle",
             "cpu": cpu_model(),
             "sample": f"first {n_problems} of {cfg.n_problems} problems ({R} rows), whole path "
-                      f"(features, forest, MLP, top-{cfg.k}, regret), {dt:.1f} s"}
+                      f"(features, forest, MLP, top-{cfg.k}, regret), {dt:.1f} s"}, parity
 
 
 def timed(torch, fn, reps: int = 3) -> float:
@@ -390,6 +399,7 @@ def main():
         },
         "measured_ceilings": ceil,
     }
+    picks = (outs[0][0].cpu().numpy(), outs[1][0].cpu().numpy())
     if not a.no_extras:
         line["extras"] = extras(a, w, hwsel, torch, dev, probs, seg, cands, rt, forest, packed, X, outs[0][0],
                                 per_stage)
@@ -400,7 +410,7 @@ def main():
             torch.cuda.empty_cache()
     if not a.no_cpu_baseline:
         log(f"cpu baseline: oracle on {a.cpu_problems} problems")
-        line["cpu_baseline"] = cpu_baseline(w, a.cpu_problems)
+        line["cpu_baseline"], line["parity"] = cpu_baseline(w, a.cpu_problems, *picks)
     print(json.dumps(line), flush=True)
 
 

@@ -393,6 +393,45 @@ def test_forest_every_depth(depth, trees, flags):
     say(f"  err/bound direct {e_direct:.3g} packed {e_packed:.3g}")
 
 
+# ----------------------------------------------------------------------------
+# the direct walk beyond the packed limits: depth 11 and 12, more than 128
+# features; packing refuses these forests with HWSEL_EUNSUPPORTED
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("depth,trees,n_features", [(11, 9, 64), (12, 5, 64), (6, 40, 200), (12, 3, 256)])
+def test_forest_direct_walk_beyond_packed_limits(depth, trees, n_features):
+    import dataclasses
+    from _gpu_util import forest_to_device
+    say(f"direct walk depth {depth} trees {trees} features {n_features}")
+    R = 5003
+    if n_features == 64:
+        cfg = dataclasses.replace(synth.CONFIGS["tiny"], trees=trees, depth=depth)
+        w = synth.workload("tiny", with_model=False)
+        f = synth.forest(cfg)
+        X = oracle.features(w.hw, w.problems, w.seg, w.cands, 64)[:R].copy()
+        rng = np.random.default_rng(depth)
+    else:
+        rng = np.random.default_rng(depth * 1000 + n_features)
+        n_int = (1 << depth) - 1
+        f = dict(n_trees=trees, depth=depth, n_features=n_features, flags=0, base_score=0.25,
+                 node_feature=rng.integers(0, n_features, (trees, n_int)).astype(np.uint8),
+                 node_threshold=rng.standard_normal((trees, n_int)).astype(np.float32),
+                 leaf_value=rng.normal(0, 0.1, (trees, 1 << depth)).astype(np.float32))
+        X = rng.standard_normal((R, n_features)).astype(np.float32)
+    X[rng.random(X.shape) < 0.02] = np.nan
+    o, oli = oracle.forest(f, X, leaves=True)
+    fd = forest_to_device(f)
+    Xd = torch.from_numpy(X).cuda()
+    g = hwsel.hwsel_forest_score(fd, Xd).cpu().numpy()
+    e = assert_forest_scores(g, o, path_l1(f, oli))
+    rows = torch.arange(0, R, 3, dtype=torch.int64, device="cuda")
+    li = hwsel.hwsel_forest_leaves(fd, Xd, rows).cpu().numpy().view(np.uint16)
+    assert np.array_equal(li, oli[::3])
+    with pytest.raises(hwsel.HwselError) as err:
+        hwsel.hwsel_forest_pack(fd)
+    assert err.value.status == hwsel.HWSEL_EUNSUPPORTED
+    say(f"  err/bound {e:.3g}; leaf indices equal on {len(rows)} rows; packing refused")
+
+
 @pytest.mark.parametrize("name", ["tiny", "dataset"])
 def test_forest_pack_host_equals_device_pack(name):
     """hwsel_forest_pack (device arrays) and hwsel_forest_pack_host (host
