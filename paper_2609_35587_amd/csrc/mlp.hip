@@ -446,13 +446,16 @@ __global__ __launch_bounds__(64 * kMWaves, 1) void k_mlp_mfma(hwsel_mlp_t m, con
                     // halfway through the epilogue (half the accumulators
                     // free), request the next tile's X
                     if (nt == 2 && g == 0) load_x(m, X, R, ld, (tile + gridDim.x) * kTile, tid, xt);
+                    // two bf16 products and their sum with the running
+                    // partial, one instruction per pair (bf16 products are
+                    // exact in fp32)
                     const uint2 w = w4[g];
                     const uint2 y = gelu_group(acc[nt], g);
                     float p = part[nt];
-                    p = fmaf(__uint_as_float(w.x << 16), __uint_as_float(y.x << 16), p);
-                    p = fmaf(__uint_as_float(w.x & 0xffff0000u), __uint_as_float(y.x & 0xffff0000u), p);
-                    p = fmaf(__uint_as_float(w.y << 16), __uint_as_float(y.y << 16), p);
-                    p = fmaf(__uint_as_float(w.y & 0xffff0000u), __uint_as_float(y.y & 0xffff0000u), p);
+                    p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, w.x), __builtin_bit_cast(bf16x2_v, y.x),
+                                                        p, false);
+                    p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, w.y), __builtin_bit_cast(bf16x2_v, y.y),
+                                                        p, false);
                     part[nt] = p;
                 }
         }
