@@ -46,18 +46,60 @@ __device__ __forceinline__ float sampling_score(int64_t clusters, int64_t cwaves
     return (float)(fill * sqrt((double)(tm * tn * tk)));
 }
 
-template <int F>
-__device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, const CandsDev &c,
-                                    int64_t r, float (&x)[F])
+// What the feature map needs of a problem alone: its integer terms and the
+// columns that depend on nothing else, computed once per problem rather than
+// once per row (the same operations, so the same values).
+struct ProbTerms {
+    int64_t M, N, K, pk, a_bytes, b_bytes, epi_traffic, conv, gemm_flops;
+    int32_t layout, dtype, eb, out_dtype;
+    // columns 0-3, 43, 46, 49, 80, 81, 88, 119-123
+    float lg_m, lg_n, lg_k, lg_flops, x43, x46, x49, x80, x81, x88, x119, x120, x121, x122, x123;
+};
+
+__device__ __forceinline__ ProbTerms problem_terms(const HwDev &h, const hwsel_problem_t &pb)
 {
-    // ---- problem ----
+    ProbTerms t;
     const int64_t M = max64(pb.M, 1), N = max64(pb.N, 1), K = max64(pb.K, 1);
-    const int layout = pb.layout < 3 ? pb.layout : 3;
     const int dtype = pb.dtype < 2 ? pb.dtype : 2;
     const int64_t eb = dtype == dFp8 ? 1 : 2;          // input element bytes (A and B)
     const int64_t ob = 2;                              // output / C element bytes
     const int out_dtype = dtype == dFp16 ? dFp16 : 0;
     const int64_t pk = h.peak[dtype];
+    t.M = M; t.N = N; t.K = K; t.pk = pk;
+    t.layout = pb.layout < 3 ? pb.layout : 3;
+    t.dtype = dtype; t.eb = (int32_t)eb; t.out_dtype = out_dtype;
+    t.a_bytes = eb * M * K;
+    t.b_bytes = eb * K * N;
+    t.epi_traffic = 2 * ob * M * N;                    // D written + C read
+    t.conv = out_dtype != dtype ? M * N * ob : 0;
+    t.gemm_flops = 2 * M * N * K;
+    t.lg_m = lg(M); t.lg_n = lg(N); t.lg_k = lg(K); t.lg_flops = lg(t.gemm_flops);
+    t.x43 = quot(t.gemm_flops, t.a_bytes + t.b_bytes + t.epi_traffic);
+    t.x46 = quot(t.a_bytes + t.b_bytes, h.llc);
+    t.x49 = exact(t.epi_traffic);
+    t.x80 = quot(pk, h.bw);
+    t.x81 = (float)(((double)t.gemm_flops / (double)(t.a_bytes + t.b_bytes + t.epi_traffic)) /
+                    ((double)pk / (double)h.bw));
+    t.x88 = exact(t.conv);
+    t.x119 = quot(t.a_bytes, h.llc);
+    t.x120 = quot(t.b_bytes, h.llc);
+    t.x121 = quot(ob * M * N, h.llc);
+    t.x122 = quot(M, N);
+    t.x123 = quot(K, max64(M, N));
+    return t;
+}
+
+template <int F>
+__device__ __forceinline__ void phi(const HwDev &h, const ProbTerms &pt, const CandsDev &c, int64_t r, float (&x)[F])
+{
+    // ---- problem ----
+    const int64_t M = pt.M, N = pt.N, K = pt.K;
+    const int layout = pt.layout;
+    const int dtype = pt.dtype;
+    const int64_t eb = pt.eb;                          // input element bytes (A and B)
+    const int64_t ob = 2;                              // output / C element bytes
+    const int out_dtype = pt.out_dtype;
+    const int64_t pk = pt.pk;
 
     // ---- candidate ----
     const int64_t tm = max64(c.tile_m[r], 1), tn = max64(c.tile_n[r], 1), tk = max64(c.tile_k[r], 1);
@@ -102,15 +144,14 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
     const int64_t cwaves = cdiv64(clusters, cslots);
 
     // ---- bytes ----
-    const int64_t a_bytes = eb * M * K, b_bytes = eb * K * N;
-    const int64_t epi_traffic = 2 * ob * M * N;        // D written + C read
+    const int64_t a_bytes = pt.a_bytes, b_bytes = pt.b_bytes;
+    const int64_t epi_traffic = pt.epi_traffic;
     const int64_t loads = gn * a_bytes + gm * b_bytes; // every tile loads its panels
-    const int64_t conv = out_dtype != dtype ? M * N * ob : 0;
-    const int64_t gemm_flops = 2 * M * N * K;
+    const int64_t conv = pt.conv;
     const int64_t tile_flops = 2 * tm * tn * tk;
 
     // ---- tier 1 ----
-    x[0] = lg(M); x[1] = lg(N); x[2] = lg(K); x[3] = lg(gemm_flops);
+    x[0] = pt.lg_m; x[1] = pt.lg_n; x[2] = pt.lg_k; x[3] = pt.lg_flops;
     x[4] = exact(tm); x[5] = exact(tn); x[6] = exact(tk); x[7] = exact(st);
     x[8] = exact(cm); x[9] = exact(cn); x[10] = exact(cm * cn); x[11] = exact(swz);
     x[12] = exact(gm); x[13] = exact(gn); x[14] = exact(gk); x[15] = exact(ntile);
@@ -141,13 +182,13 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
     x[40] = quot(gm, cm);
     x[41] = quot(gn, cn);
     x[42] = exact((cm > gm || cn > gn) ? 1 : 0);
-    x[43] = quot(gemm_flops, a_bytes + b_bytes + epi_traffic);
+    x[43] = pt.x43;
     x[44] = quot(2 * tm * tn, (tm + tn) * eb);
     x[45] = quot(loads, a_bytes + b_bytes);
-    x[46] = quot(a_bytes + b_bytes, h.llc);
+    x[46] = pt.x46;
     x[47] = quot((tm + tn) * K * eb, h.llc);
     x[48] = exact(loads);
-    x[49] = exact(epi_traffic);
+    x[49] = pt.x49;
     const double t_load = (double)(h.n_sm * stage_bytes) / (double)h.bw;
     const double t_mma = (double)(tile_flops * h.n_sm) / (double)(consumers * pk);
     x[50] = quot(h.n_sm * stage_bytes, h.bw);
@@ -173,9 +214,8 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
         x[70] = exact(eb); x[71] = exact(eb); x[72] = exact(ob);
         x[73] = exact(ks); x[74] = exact(es); x[75] = exact(ts); x[76] = exact(streamk);
         x[77] = exact(consumers); x[78] = exact(h.arch_id); x[79] = exact(pk);
-        x[80] = quot(pk, h.bw);
-        x[81] = (float)(((double)gemm_flops / (double)(a_bytes + b_bytes + epi_traffic)) /
-                        ((double)pk / (double)h.bw));
+        x[80] = pt.x80;
+        x[81] = pt.x81;
         const bool ok_a = !a_colmajor || tk <= 256 * cn;
         const bool ok_b = !b_rowmajor || tk <= 256 * cm;
         const bool ok_coop = ks != kCoop || (tm % 128) == 0;
@@ -183,7 +223,7 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
         x[82] = exact(ok_a); x[83] = exact(ok_b); x[84] = exact(ok_coop); x[85] = exact(ok_sk);
         x[86] = exact(tn <= 2 * M && tn <= 2 * N);
         x[87] = exact(fits && ok_a && ok_b && ok_coop && ok_sk);
-        x[88] = exact(conv);
+        x[88] = pt.x88;
         const int64_t traffic = loads + epi_traffic + conv;
         x[89] = exact(traffic);
         x[90] = quot(traffic, h.bw);
@@ -212,11 +252,11 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
         x[116] = exact(resident * threads);
         x[117] = quot(resident * threads, h.threads_sm_max);
         x[118] = exact(by_arch == resident);
-        x[119] = quot(a_bytes, h.llc);
-        x[120] = quot(b_bytes, h.llc);
-        x[121] = quot(ob * M * N, h.llc);
-        x[122] = quot(M, N);
-        x[123] = quot(K, max64(M, N));
+        x[119] = pt.x119;
+        x[120] = pt.x120;
+        x[121] = pt.x121;
+        x[122] = pt.x122;
+        x[123] = pt.x123;
         x[124] = quot(clusters, cslots);
         const int64_t edge = ntile - (M / tm) * (N / tn);
         x[125] = exact(edge);
@@ -226,12 +266,16 @@ __device__ __forceinline__ void phi(const HwDev &h, const hwsel_problem_t &pb, c
 }
 
 constexpr int kWaves = 4;
+constexpr int kCachedProblems = 4;
 
 // One row per thread.  The row's columns are produced 64 (or 32) at a time:
 // each pass evaluates the feature map and keeps only its columns (the shared
 // integer intermediates are recomputed, the per-column work is not), which
 // keeps the live registers low enough for more than one wave per SIMD.  Each
-// 32-column slab is transposed through LDS into 16-byte row stores.
+// 32-column slab is transposed through LDS into 16-byte row stores.  The
+// problem terms of the workgroup's first problems (usually its only one) are
+// computed once, by the first threads, and read from LDS by every row; rows
+// of a later problem compute their own.
 template <int F>
 __global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_problem_t *__restrict__ probs,
                                                           int32_t P, const int64_t *__restrict__ seg,
@@ -239,11 +283,24 @@ __global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_p
                                                           int64_t ld)
 {
     __shared__ float stage[kWaves][64][33];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t row0 = ((int64_t)blockIdx.x * kWaves + wave) * 64;
+    __shared__ ProbTerms cached[kCachedProblems];
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t blk0 = (int64_t)blockIdx.x * kWaves * 64;            // < R
+    const int64_t row0 = blk0 + wave * 64;
     const int64_t r = row0 + lane;
+    const int32_t p0 = segment_of_row(seg, P, blk0);
+    const int32_t p_end = segment_of_row(seg, P, min64(blk0 + 64 * kWaves, R) - 1) + 1;
+    const int n_cached = p_end - p0 < kCachedProblems ? p_end - p0 : kCachedProblems;
+    if ((int)threadIdx.x < n_cached) cached[threadIdx.x] = problem_terms(h, probs[p0 + threadIdx.x]);
     hwsel_problem_t pb{};
-    if (r < R) pb = probs[segment_of_row(seg, P, r)];
+    int slot = -1;                                     // index into cached, or -1
+    if (r < R) {
+        // the wave's rows are consecutive: one scalar search for its first row
+        const int32_t p = segment_of_row_after(seg, P, r, row0);
+        if (p - p0 < n_cached) slot = p - p0;
+        else pb = probs[p];
+    }
+    __syncthreads();
     constexpr int kPass = F % 64 == 0 ? 64 : 32;      // columns per evaluation of the map
     float xs[kPass];
 #pragma unroll
@@ -251,7 +308,11 @@ __global__ __launch_bounds__(64 * kWaves) void k_features(HwDev h, const hwsel_p
         if (ch % (kPass / 32) == 0) {
             float x[F];
             if (r < R) {
-                phi<F>(h, pb, c, r, x);
+                // re-read per pass rather than held across passes
+                int sl = slot;
+                asm volatile("" : "+v"(sl));
+                const ProbTerms pt = sl >= 0 ? cached[sl] : problem_terms(h, pb);
+                phi<F>(h, pt, c, r, x);
             } else {
 #pragma unroll
                 for (int j = 0; j < F; ++j) x[j] = 0.0f;
@@ -341,7 +402,7 @@ __global__ __launch_bounds__(kFbThreads, 1) void k_features_bins(HwDev h, const 
             int64_t rp = r;
             asm volatile("" : "+v"(rp));
             float x[F];
-            phi<F>(h, pb, c, rp, x);
+            phi<F>(h, problem_terms(h, pb), c, rp, x);
             // kFbChains independent searches in flight
 #pragma unroll
             for (int f0 = p0; f0 < p0 + kPass; f0 += kFbChains) {

@@ -42,6 +42,27 @@ def test_features_tiny_all_rows(tiny):
     say(f"  {compare_features(X, ref, 64)}")
 
 
+@pytest.mark.parametrize("F", [64, 96, 128])
+def test_features_ragged_segments(tiny, F):
+    """Segments of 0 to 300 rows: workgroups of 256 rows that span many
+    problems (more than the kernel computes problem terms for once), problems
+    that change inside a wave, empty segments; every row and column against
+    the oracle."""
+    w, _ = tiny
+    rng = np.random.default_rng(F)
+    lengths = rng.choice([0, 0, 1, 2, 3, 5, 17, 63, 64, 65, 130, 300], size=160)
+    lengths = lengths[np.cumsum(lengths) <= len(w.cands["tile_m"])]
+    seg = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    R = int(seg[-1])
+    probs = w.problems[rng.integers(0, len(w.problems), len(lengths))]
+    cands = {k: np.ascontiguousarray(v[:R]) for k, v in w.cands.items()}
+    say(f"features ragged F={F}: {len(lengths)} problems, {R} rows")
+    X = hwsel.hwsel_features(w.hw, hwsel.to_device(probs), hwsel.to_device(seg),
+                             {k: hwsel.to_device(v) for k, v in cands.items()}, F).cpu().numpy()
+    ref = oracle.features(w.hw, probs, seg, cands, F)
+    say(f"  {compare_features(X, ref, F)}")
+
+
 def test_forest_tiny_all_rows(tiny):
     w, d = tiny
     say("forest tiny")
