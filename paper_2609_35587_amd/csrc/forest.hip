@@ -394,11 +394,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const void *__restr
         const uint32_t p1 = D >= 2 ? *reinterpret_cast<const uint32_t *>(lds + ROW_B + col) : 0u;
         const uint32_t p2 = D >= 3 ? *reinterpret_cast<const uint32_t *>(lds + 2 * ROW_B + col) : 0u;
         const uint32_t p3 = D >= 3 ? *reinterpret_cast<const uint32_t *>(lds + 3 * ROW_B + col) : 0u;
-        uint4 pre[kVec];
+        uint4 preA[kVec], preB[kVec];
         const bool full_rows = stride == 128;              // wave-uniform
         // A lane's byte offsets within its wave's slice are the same for every
         // tile; only whole slices inside the row range skip the row guards.
-        auto fetch = [&](int64_t t0) {
+        auto fetch = [&](int64_t t0, uint4 (&pre)[kVec]) {
             const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
             const uint8_t *slice = Xb + w0 * stride;       // wave-uniform
             if (full_rows && w0 + ROWS_PER_WAVE <= r_end) {
@@ -421,8 +421,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const void *__restr
                 }
             }
         };
-        fetch(r_begin);
-        for (int64_t t0 = r_begin; t0 < r_end; t0 += kTileRows) {
+        // Two tiles in flight: a tile's bins are requested two tiles before
+        // they are written to LDS, alternating between two register buffers.
+        fetch(r_begin, preA);
+        fetch(r_begin + kTileRows, preB);
+        auto tile = [&](int64_t t0, uint4 (&pre)[kVec]) {
             const int64_t w0 = t0 + wave * ROWS_PER_WAVE;
             // The previous rows' reads have all returned (their results were
             // used), so the region can be overwritten.
@@ -449,8 +452,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const void *__restr
                 }
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the region is written before any lane reads it
-            fetch(t0 + kTileRows);
-            if (w0 >= r_end) continue;                               // wave-uniform: no rows left here
+            fetch(t0 + 2 * kTileRows, pre);
+            if (w0 >= r_end) return;                                 // wave-uniform: no rows left here
 #pragma unroll 1
             for (int it = 0; it < ITER; ++it) {
                 int node[ILP];
@@ -517,6 +520,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_traverse(const void *__restr
                         if (w0 + (it * ILP + a) * RPI + s < r_end) out[a * RPI] = v[a];
                 }
             }
+        };
+        for (int64_t t0 = r_begin; t0 < r_end; t0 += 2 * kTileRows) {
+            tile(t0, preA);
+            if (t0 + kTileRows < r_end) tile(t0 + kTileRows, preB);
         }
     }
 }
@@ -561,11 +568,35 @@ __global__ __launch_bounds__(256) void k_reduce4(const void *__restrict__ packed
     *reinterpret_cast<float4 *>(scores + r) = acc;
 }
 
+// Row groups per XCD.  The XCD's kSlotsPerXcd workgroups take (chunk, group)
+// items in turn.  With fewer chunks than workgroups: enough groups for one
+// round.  Otherwise n_chunks * groups items should fill whole rounds: the
+// fewest groups that leave under 0.5 % of the rounds' slots idle, else the
+// one that leaves fewest, among those that still give every group at least
+// four row tiles (125 chunks of a 4.9 M-row call: 11 groups, 1,375 items in
+// 43 rounds of 32).
+inline int groups_per_xcd(int n_chunks, int64_t R, int tile)
+{
+    if (n_chunks < kSlotsPerXcd) return (kSlotsPerXcd + n_chunks - 1) / n_chunks;
+    const int64_t cap_rows = R / ((int64_t)kXcds * tile * 4);
+    const int cap = cap_rows < 1 ? 1 : cap_rows > kSlotsPerXcd ? kSlotsPerXcd : (int)cap_rows;
+    int best = 1;
+    double best_idle = 1.0;
+    for (int g = 1; g <= cap; ++g) {
+        const int64_t items = (int64_t)n_chunks * g;
+        const int64_t slots = (items + kSlotsPerXcd - 1) / kSlotsPerXcd * kSlotsPerXcd;
+        const double idle = (double)(slots - items) / (double)slots;
+        if (idle < 0.005) return g;
+        if (idle < best_idle) best_idle = idle, best = g;
+    }
+    return best;
+}
+
 template <int TC, int D>
 hipError_t launch_traverse_tc(const void *packed, ImageId id, const uint8_t *chunks, int n_chunks, const uint8_t *Xb,
                               int64_t R, int stride, float *partial, const LeafHook &hook, hipStream_t s)
 {
-    const int groups = n_chunks >= kSlotsPerXcd ? 1 : (kSlotsPerXcd + n_chunks - 1) / n_chunks;
+    const int groups = groups_per_xcd(n_chunks, R, tile_rows(TC));
     const int64_t n_groups = (int64_t)kXcds * groups;
     int64_t per = (R + n_groups - 1) / n_groups;
     per = (per + tile_rows(TC) - 1) / tile_rows(TC) * tile_rows(TC);
